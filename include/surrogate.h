@@ -1,0 +1,182 @@
+/*
+ * surrogate.h - C ABI of the batched forecast-scoring library (libsurrogate.so).
+ *
+ * The library scores forecast queries with a dense decoder-only transformer in a
+ * prefill-only pass on one MI355X (gfx950).  A query is the tokenized prompt of
+ * x_i = (reference kernel, candidate kernel, hardware) from Section 2.1 of the paper
+ * (Forecasting Relative Performance).  At the last prompt position the model's
+ * next-token log-probabilities of a fixed set of verdict tokens give a forecast
+ * distribution p_i, a predicted verdict (argmax) and a confidence q_i = max_b p_{i,b}
+ * (Section 2.1).  Selective use (Section 2.1, Selective Use; budgeted measurement in
+ * Section 3.1) then splits a batch into forecasts to accept and candidates to defer
+ * to GPU measurement.
+ *
+ * Conventions shared by every call:
+ *  - Every call returns a surrogate_status; 0 is success, negative values are errors.
+ *    On error, surrogate_last_error() returns a thread-local description.
+ *  - Pointers suffixed _d are device pointers, _h host pointers.  The caller owns every
+ *    buffer it passes; the library keeps no pointer to them after the call returns
+ *    (device work stays stream-ordered: buffers must stay valid until the stream has
+ *    passed the call's work).
+ *  - Device work is enqueued on the caller's stream and is asynchronous.  Host-checkable
+ *    argument errors are reported synchronously and then nothing is enqueued.
+ *  - A model handle is read-only after loading; concurrent calls on one handle are
+ *    allowed only with distinct workspaces and output buffers.
+ */
+#ifndef SURROGATE_H
+#define SURROGATE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SURR_OK = 0,
+    SURR_E_INVALID_ARG = -1, /* null pointer, bad count, bad mode, bad threshold/budget */
+    SURR_E_SHAPE = -2,       /* config shape unsupported, or a length outside [1, limit] */
+    SURR_E_TOKEN_RANGE = -3, /* a token id outside [0, vocab) was seen on the device   */
+    SURR_E_OOM = -4,         /* device or pinned host allocation failed                  */
+    SURR_E_HIP = -5,         /* a HIP runtime call failed                                */
+    SURR_E_WEIGHTS = -6,     /* weight tensor list does not match the config             */
+    SURR_E_WORKSPACE = -7    /* workspace smaller than surrogate_workspace_size()        */
+} surrogate_status;
+
+typedef enum { SURR_F32 = 0, SURR_BF16 = 1 } surrogate_dtype;
+
+typedef enum { SURR_SELECT_THRESHOLD = 0, SURR_SELECT_BUDGET = 1 } surrogate_select_mode;
+
+typedef struct surrogate_model surrogate_model; /* opaque: device weights + RoPE table */
+
+/* Architecture of the decoder: pre-norm RMSNorm, rotate-half RoPE, causal grouped-
+ * query attention (query head a reads kv head floor(a * n_kv_heads / n_q_heads)),
+ * SwiGLU MLP, final RMSNorm and an untied LM head, no biases.
+ * dtype selects the storage and GEMM-input type of the matrices (SURR_F32 or
+ * SURR_BF16); norm gains are always float32.  Supported shapes: head_dim in
+ * {32, 64, 128}; d_model, d_ff and head_dim*n_q_heads multiples of 64 (bf16) or of 32
+ * (f32); n_q_heads a multiple of n_kv_heads; max_pos >= 1. */
+typedef struct {
+    int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ff, vocab, max_pos;
+    float rope_base, rms_eps;
+    int32_t dtype;
+} surrogate_config;
+
+/* Number of weight tensors for cfg: 3 + 9 * n_layers. */
+surrogate_status surrogate_tensor_count(const surrogate_config *cfg, int32_t *n_out);
+
+/* Shape and element type of tensor `index` in the canonical order
+ *   embed[V, d];
+ *   per layer: attn_norm[d], w_q[d_q, d], w_k[d_kv, d], w_v[d_kv, d], w_o[d, d_q],
+ *              mlp_norm[d], w_gate[d_ff, d], w_up[d_ff, d], w_down[d, d_ff];
+ *   final_norm[d]; lm_head[V, d]
+ * (d_q = n_q_heads * head_dim, d_kv = n_kv_heads * head_dim).  Matrices are row-major
+ * [out, in]; norms are reported as rows = 1.  *dtype_out is SURR_F32 for norms and
+ * cfg->dtype for matrices (bf16 = raw 16-bit patterns). */
+surrogate_status surrogate_tensor_shape(const surrogate_config *cfg, int32_t index,
+                                        int64_t *rows, int64_t *cols, int32_t *dtype_out);
+
+/* Create a model from the n_tensors = surrogate_tensor_count() tensors in canonical
+ * order.  tensors[i] points to a dense row-major tensor of surrogate_tensor_shape(i);
+ * all of them are host memory if tensors_on_device == 0, device memory otherwise.
+ * The library copies them into its own device arena (re-laid out for its kernels),
+ * builds the RoPE cos/sin table in float64 and stores it as float32, and synchronizes
+ * `stream` before returning, so the sources may be freed afterwards.
+ * Errors: SURR_E_INVALID_ARG (nulls), SURR_E_SHAPE (unsupported config),
+ * SURR_E_WEIGHTS (n_tensors mismatch), SURR_E_OOM, SURR_E_HIP. */
+surrogate_status surrogate_load_weights(const surrogate_config *cfg, const void *const *tensors,
+                                        int32_t n_tensors, int32_t tensors_on_device,
+                                        hipStream_t stream, surrogate_model **out);
+
+surrogate_status surrogate_get_config(const surrogate_model *m, surrogate_config *out);
+
+/* Device workspace (bytes) that surrogate_score_pairs needs for a batch of `batch`
+ * prompts holding `total_tokens` tokens in all, none longer than `max_len`. */
+surrogate_status surrogate_workspace_size(const surrogate_model *m, int32_t batch,
+                                          int64_t total_tokens, int32_t max_len, size_t *bytes);
+
+/* Score a ragged batch (the prefill-only surrogate call).
+ *  tokens_d      device int32 [batch, row_stride]; row i holds prompt i in its first
+ *                lengths_h[i] entries; entries beyond are never read.
+ *  lengths_h     host int32 [batch]; 1 <= lengths_h[i] <= min(row_stride, max_pos).
+ *  verdict_ids_h host int32 [n_verdict], 1 <= n_verdict <= 16, distinct ids in [0, vocab).
+ *  workspace_d   device buffer of >= surrogate_workspace_size() bytes, 256-byte aligned.
+ * Outputs (device, caller-owned):
+ *  logprobs_d    float [batch, n_verdict]: log-softmax over the full vocabulary of the
+ *                next-token logits at position lengths_h[i] - 1, at the verdict ids.
+ *  probs_d       float [batch, n_verdict] or NULL: p_i = softmax of those log-probs.
+ *  confidence_d  float [batch]: q_i = max_b p_{i,b}.
+ *  verdict_d     int32 [batch] or NULL: argmax_b p_{i,b}, lowest index on ties.
+ * A token id outside [0, vocab) is read as id 0 and raises a sticky device error that
+ * surrogate_device_status() reports as SURR_E_TOKEN_RANGE.  Results are deterministic:
+ * a prompt's outputs do not depend on the other prompts of the batch or on the run.
+ * Errors (synchronous, nothing enqueued): SURR_E_INVALID_ARG, SURR_E_SHAPE,
+ * SURR_E_WORKSPACE, SURR_E_OOM (pinned staging), SURR_E_HIP. */
+surrogate_status surrogate_score_pairs(surrogate_model *m, const int32_t *tokens_d,
+                                       int64_t row_stride, const int32_t *lengths_h,
+                                       int32_t batch, const int32_t *verdict_ids_h,
+                                       int32_t n_verdict, void *workspace_d,
+                                       size_t workspace_bytes, float *logprobs_d, float *probs_d,
+                                       float *confidence_d, int32_t *verdict_d,
+                                       hipStream_t stream);
+
+/* Selective deferral on a device confidence vector confidence_d[n], 1 <= n <= 65536.
+ *  SURR_SELECT_THRESHOLD: accept i iff confidence[i] >= threshold in float32 (the
+ *    convention s >= tau of Section 3.6); NaN is never accepted.  budget_k is ignored.
+ *  SURR_SELECT_BUDGET: defer the min(budget_k, n) candidates of lowest confidence
+ *    (Section 3.1 measures a budgeted subset); order is confidence ascending with NaN
+ *    first, ties by ascending index, -0.0 == +0.0.  budget_k < 0 is an error.
+ * Outputs (device): defer_idx_d[n] and accept_idx_d[n] receive the ascending index
+ * lists (entries past each count are left untouched); counts_d[2] = {n_defer,
+ * n_accept}, which sum to n.  Bit-exact and deterministic. */
+surrogate_status surrogate_select(const float *confidence_d, int32_t n,
+                                  surrogate_select_mode mode, float threshold, int32_t budget_k,
+                                  int32_t *defer_idx_d, int32_t *accept_idx_d, int32_t *counts_d,
+                                  hipStream_t stream);
+
+/* Synchronize `stream` and report (then clear) the sticky device error of the model:
+ * SURR_E_TOKEN_RANGE if an out-of-range token id was seen since the last check. */
+surrogate_status surrogate_device_status(surrogate_model *m, hipStream_t stream);
+
+/* Measurement hook.  Kernel phases of surrogate_score_pairs: */
+typedef enum {
+    SURR_PHASE_EMBED = 0,     /* varlen token packing + embedding gather          */
+    SURR_PHASE_RMSNORM,       /* every RMSNorm (attention, MLP, final)             */
+    SURR_PHASE_GEMM_QKV,      /* fused QKV projection                              */
+    SURR_PHASE_ROPE,          /* rotary embedding of q and k                       */
+    SURR_PHASE_ATTENTION,     /* causal GQA prefill attention                      */
+    SURR_PHASE_GEMM_O,        /* output projection + residual                      */
+    SURR_PHASE_GEMM_GATE_UP,  /* gate/up projection + SwiGLU                       */
+    SURR_PHASE_GEMM_DOWN,     /* down projection + residual                        */
+    SURR_PHASE_GATHER,        /* last-position row gathers                         */
+    SURR_PHASE_LM_HEAD,       /* last-position LM head GEMM                        */
+    SURR_PHASE_LSE_VERDICT,   /* full-vocab log-softmax + verdict read-out         */
+    SURR_N_PHASES
+} surrogate_phase;
+
+/* While enabled (enable != 0), surrogate_score_pairs brackets every kernel launch with
+ * a pair of HIP events on its stream.  surrogate_profile_collect synchronizes those
+ * events, writes per-phase totals since the previous collect (ms_out[SURR_N_PHASES]
+ * milliseconds, launches_out[SURR_N_PHASES] launch counts) and resets them.  Not for
+ * concurrent use on one model.  Errors: SURR_E_INVALID_ARG, SURR_E_HIP. */
+surrogate_status surrogate_profile_enable(surrogate_model *m, int32_t enable);
+surrogate_status surrogate_profile_collect(surrogate_model *m, double *ms_out,
+                                           int64_t *launches_out);
+
+/* Release the model's device memory.  Pending work that uses the model must have
+ * completed.  NULL is ignored. */
+void surrogate_free(surrogate_model *m);
+
+const char *surrogate_status_string(surrogate_status s);
+
+/* Thread-local detail of the last failing call on this thread ("" if none). */
+const char *surrogate_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SURROGATE_H */

@@ -1,0 +1,266 @@
+"""ctypes binding of libsurrogate.so: the C ABI of include/surrogate.h under the same names.
+
+Argument marshalling only: torch tensors supply device memory and the current HIP
+stream; every step of scoring and selection runs in the library's HIP kernels.  There
+is no CPU fallback - loading fails loudly when the library is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libsurrogate.so")
+
+SURR_OK = 0
+SURR_E_INVALID_ARG = -1
+SURR_E_SHAPE = -2
+SURR_E_TOKEN_RANGE = -3
+SURR_E_OOM = -4
+SURR_E_HIP = -5
+SURR_E_WEIGHTS = -6
+SURR_E_WORKSPACE = -7
+SURR_F32, SURR_BF16 = 0, 1
+SURR_SELECT_THRESHOLD, SURR_SELECT_BUDGET = 0, 1
+
+EXPORTS = ("surrogate_tensor_count", "surrogate_tensor_shape", "surrogate_load_weights",
+           "surrogate_get_config", "surrogate_workspace_size", "surrogate_score_pairs",
+           "surrogate_select", "surrogate_device_status", "surrogate_free",
+           "surrogate_status_string", "surrogate_last_error", "surrogate_profile_enable",
+           "surrogate_profile_collect")
+PHASES = ("embed", "rmsnorm", "gemm_qkv", "rope", "attention", "gemm_o", "gemm_gate_up",
+          "gemm_down", "gather", "lm_head", "lse_verdict")
+
+
+class SurrogateError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status} ({detail})")
+        self.status = status
+
+
+class surrogate_config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("n_layers", "d_model", "n_q_heads", "n_kv_heads", "head_dim", "d_ff", "vocab",
+                 "max_pos")] + [("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float),
+                                ("dtype", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsurrogate.so (built by build_lib); raise if it is not there."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2605_31464_amd.build_lib` (no CPU fallback exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+    cfgp = ctypes.POINTER(surrogate_config)
+    sig = {
+        "surrogate_tensor_count": (I32, [cfgp, ctypes.POINTER(I32)]),
+        "surrogate_tensor_shape": (I32, [cfgp, I32, ctypes.POINTER(I64), ctypes.POINTER(I64),
+                                         ctypes.POINTER(I32)]),
+        "surrogate_load_weights": (I32, [cfgp, ctypes.POINTER(P), I32, I32, P, ctypes.POINTER(P)]),
+        "surrogate_get_config": (I32, [P, cfgp]),
+        "surrogate_workspace_size": (I32, [P, I32, I64, I32, ctypes.POINTER(SZ)]),
+        "surrogate_score_pairs": (I32, [P, P, I64, P, I32, P, I32, P, SZ, P, P, P, P, P]),
+        "surrogate_select": (I32, [P, I32, I32, F, I32, P, P, P, P]),
+        "surrogate_device_status": (I32, [P, P]),
+        "surrogate_free": (None, [P]),
+        "surrogate_status_string": (ctypes.c_char_p, [I32]),
+        "surrogate_last_error": (ctypes.c_char_p, []),
+        "surrogate_profile_enable": (I32, [P, I32]),
+        "surrogate_profile_collect": (I32, [P, P, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype, fn.argtypes = res, args
+    _lib = L
+    return L
+
+
+def _check(status: int, where: str):
+    if status != SURR_OK:
+        L = lib()
+        raise SurrogateError(status, where, L.surrogate_last_error().decode())
+
+
+def make_config(shape) -> surrogate_config:
+    """surrogate_config from an object with the ModelShape fields."""
+    return surrogate_config(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
+                            shape.head_dim, shape.d_ff, shape.vocab, shape.max_pos,
+                            float(shape.rope_base), float(shape.rms_eps),
+                            SURR_BF16 if shape.dtype == "bf16" else SURR_F32)
+
+
+def _stream(stream=None) -> int:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return int(s.cuda_stream)
+
+
+def surrogate_tensor_count(cfg: surrogate_config) -> int:
+    n = ctypes.c_int32()
+    _check(lib().surrogate_tensor_count(ctypes.byref(cfg), ctypes.byref(n)), "surrogate_tensor_count")
+    return n.value
+
+
+def surrogate_tensor_shape(cfg: surrogate_config, index: int):
+    r, c, dt = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int32()
+    _check(lib().surrogate_tensor_shape(ctypes.byref(cfg), index, ctypes.byref(r), ctypes.byref(c),
+                                        ctypes.byref(dt)), "surrogate_tensor_shape")
+    return r.value, c.value, dt.value
+
+
+class Model:
+    """Owns a surrogate_model handle (device weights)."""
+
+    def __init__(self, handle: int, cfg: surrogate_config):
+        self.handle = ctypes.c_void_p(handle)
+        self.cfg = cfg
+
+    def close(self):
+        if self.handle:
+            lib().surrogate_free(self.handle)
+            self.handle = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def surrogate_load_weights(cfg: surrogate_config, tensors, stream=None) -> Model:
+    """tensors: canonical-order list of numpy host arrays or torch device tensors."""
+    n = len(tensors)
+    on_device = 0
+    ptrs = (ctypes.c_void_p * n)()
+    keep = []
+    for i, t in enumerate(tensors):
+        rows, cols, dt = surrogate_tensor_shape(cfg, i)
+        if isinstance(t, np.ndarray):
+            a = np.ascontiguousarray(t)
+            want = np.float32 if dt == SURR_F32 else np.uint16
+            if a.dtype != want or a.size != rows * cols:
+                raise ValueError(f"tensor {i}: want {want.__name__} x {rows * cols}, got {a.dtype} x {a.size}")
+            keep.append(a)
+            ptrs[i] = a.ctypes.data
+        else:
+            on_device = 1
+            if not t.is_contiguous() or t.numel() != rows * cols:
+                raise ValueError(f"tensor {i}: need a contiguous device tensor of {rows * cols} elements")
+            keep.append(t)
+            ptrs[i] = t.data_ptr()
+    if on_device and any(isinstance(t, np.ndarray) for t in tensors):
+        raise ValueError("tensors must be all host arrays or all device tensors")
+    h = ctypes.c_void_p()
+    _check(lib().surrogate_load_weights(ctypes.byref(cfg), ptrs, n, on_device,
+                                        ctypes.c_void_p(_stream(stream)), ctypes.byref(h)),
+           "surrogate_load_weights")
+    return Model(h.value, cfg)
+
+
+def surrogate_workspace_size(model: Model, batch: int, total_tokens: int, max_len: int) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().surrogate_workspace_size(model.handle, batch, total_tokens, max_len,
+                                          ctypes.byref(out)), "surrogate_workspace_size")
+    return out.value
+
+
+def surrogate_score_pairs(model: Model, tokens, lengths, verdict_ids, workspace, logprobs,
+                          confidence, probs=None, verdict=None, stream=None):
+    """tokens: int32 device [B, S]; lengths, verdict_ids: host int sequences;
+    workspace: device byte tensor; outputs: preallocated device tensors."""
+    import torch
+    if tokens.dtype != torch.int32 or tokens.dim() != 2 or not tokens.is_contiguous():
+        raise ValueError("tokens must be a contiguous int32 [B, S] device tensor")
+    L = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
+    vid = np.ascontiguousarray(np.asarray(verdict_ids, dtype=np.int32))
+    B = int(tokens.shape[0])
+    if L.shape != (B,):
+        raise ValueError("lengths must have one entry per row of tokens")
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
+    _check(lib().surrogate_score_pairs(
+        model.handle, ptr(tokens), int(tokens.shape[1]), L.ctypes.data_as(ctypes.c_void_p), B,
+        vid.ctypes.data_as(ctypes.c_void_p), int(vid.size), ptr(workspace),
+        workspace.numel() * workspace.element_size(), ptr(logprobs), ptr(probs), ptr(confidence),
+        ptr(verdict), ctypes.c_void_p(_stream(stream))), "surrogate_score_pairs")
+
+
+def surrogate_select(confidence, mode: int, threshold: float = 0.0, budget_k: int = 0,
+                     defer_idx=None, accept_idx=None, counts=None, stream=None):
+    """Returns (defer_idx, accept_idx, counts) device int32 tensors."""
+    import torch
+    n = int(confidence.numel())
+    dev = confidence.device
+    defer_idx = torch.empty(n, dtype=torch.int32, device=dev) if defer_idx is None else defer_idx
+    accept_idx = torch.empty(n, dtype=torch.int32, device=dev) if accept_idx is None else accept_idx
+    counts = torch.empty(2, dtype=torch.int32, device=dev) if counts is None else counts
+    _check(lib().surrogate_select(ctypes.c_void_p(confidence.data_ptr()), n, mode, float(threshold),
+                                  int(budget_k), ctypes.c_void_p(defer_idx.data_ptr()),
+                                  ctypes.c_void_p(accept_idx.data_ptr()),
+                                  ctypes.c_void_p(counts.data_ptr()),
+                                  ctypes.c_void_p(_stream(stream))), "surrogate_select")
+    return defer_idx, accept_idx, counts
+
+
+def surrogate_device_status(model: Model, stream=None) -> int:
+    """Synchronizes; returns SURR_OK or SURR_E_TOKEN_RANGE (sticky flag, then cleared)."""
+    return lib().surrogate_device_status(model.handle, ctypes.c_void_p(_stream(stream)))
+
+
+def surrogate_profile_enable(model: Model, enable: bool = True):
+    _check(lib().surrogate_profile_enable(model.handle, int(bool(enable))), "surrogate_profile_enable")
+
+
+def surrogate_profile_collect(model: Model) -> dict:
+    """{phase: (milliseconds, launches)} since the previous collect."""
+    ms = (ctypes.c_double * len(PHASES))()
+    n = (ctypes.c_int64 * len(PHASES))()
+    _check(lib().surrogate_profile_collect(model.handle, ms, n), "surrogate_profile_collect")
+    return {p: (ms[i], n[i]) for i, p in enumerate(PHASES)}
+
+
+def surrogate_free(model: Model):
+    model.close()
+
+
+# ---------------------------------------------------------------- convenience layer
+class Scorer:
+    """A loaded model plus a workspace sized for one batch shape."""
+
+    def __init__(self, shape, weights: dict, names, device="cuda:0"):
+        import torch
+        self.torch = torch
+        self.device = torch.device(device)
+        self.cfg = make_config(shape)
+        with torch.cuda.device(self.device):
+            self.model = surrogate_load_weights(self.cfg, [weights[n] for n in names])
+        self.workspace = None
+
+    def ensure_workspace(self, batch, total_tokens, max_len):
+        need = surrogate_workspace_size(self.model, batch, total_tokens, max_len)
+        if self.workspace is None or self.workspace.numel() < need:
+            self.workspace = None
+            self.workspace = self.torch.empty(need, dtype=self.torch.uint8, device=self.device)
+        return self.workspace
+
+    def score(self, tokens, lengths, verdict_ids):
+        torch = self.torch
+        tok = torch.as_tensor(np.asarray(tokens, np.int32)).to(self.device) \
+            if not isinstance(tokens, torch.Tensor) else tokens
+        L = np.asarray(lengths, np.int32)
+        B, nv = len(L), len(verdict_ids)
+        ws = self.ensure_workspace(B, int(L.sum()), int(L.max()))
+        out = {"logprobs": torch.empty(B, nv, dtype=torch.float32, device=self.device),
+               "p": torch.empty(B, nv, dtype=torch.float32, device=self.device),
+               "confidence": torch.empty(B, dtype=torch.float32, device=self.device),
+               "verdict": torch.empty(B, dtype=torch.int32, device=self.device)}
+        surrogate_score_pairs(self.model, tok, L, verdict_ids, ws, out["logprobs"], out["confidence"],
+                              out["p"], out["verdict"])
+        return out

@@ -1,0 +1,344 @@
+// Bandwidth-bound kernels: embedding gather, RMSNorm, RoPE, fp32 SwiGLU, row gather,
+// full-vocab log-softmax + verdict read-out, and selective deferral.
+#include "common.h"
+#include "kernels.h"
+
+namespace surr {
+namespace {
+
+// ---------------------------------------------------------------- embedding gather
+// One wavefront per packed token t: find its prompt b (cu[b] <= t < cu[b+1]) by binary
+// search, read the token id, and widen the embedding row to the fp32 residual.
+template <bool BF16>
+__global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ tokens,
+                                                    int64_t row_stride,
+                                                    const int32_t* __restrict__ cu, int B,
+                                                    int64_t T, const void* __restrict__ embed,
+                                                    int d, int vocab, float* __restrict__ x,
+                                                    int32_t* __restrict__ pos,
+                                                    int32_t* __restrict__ err_flag) {
+    const int lane = threadIdx.x & 63;
+    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (t >= T) return;
+    int lo = 0, hi = B;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (cu[mid] <= t) lo = mid; else hi = mid;
+    }
+    const int j = (int)(t - cu[lo]);
+    int tok = tokens[(int64_t)lo * row_stride + j];
+    if (tok < 0 || tok >= vocab) {
+        if (lane == 0) err_flag[0] = 1;
+        tok = 0;
+    }
+    if (lane == 0) pos[t] = j;
+    float4* xr = reinterpret_cast<float4*>(x + t * d);
+    if constexpr (BF16) {
+        const uint4* er = reinterpret_cast<const uint4*>(
+            static_cast<const uint16_t*>(embed) + (int64_t)tok * d);
+        for (int c = lane; c < d / 8; c += 64) {
+            const uint4 v = er[c];
+            xr[2 * c] = make_float4(bf16_to_f32(v.x & 0xffffu), bf16_to_f32(v.x >> 16),
+                                    bf16_to_f32(v.y & 0xffffu), bf16_to_f32(v.y >> 16));
+            xr[2 * c + 1] = make_float4(bf16_to_f32(v.z & 0xffffu), bf16_to_f32(v.z >> 16),
+                                        bf16_to_f32(v.w & 0xffffu), bf16_to_f32(v.w >> 16));
+        }
+    } else {
+        const float4* er = reinterpret_cast<const float4*>(
+            static_cast<const float*>(embed) + (int64_t)tok * d);
+        for (int c = lane; c < d / 4; c += 64) xr[c] = er[c];
+    }
+}
+
+// ---------------------------------------------------------------- RMSNorm
+// One wavefront per row; fp32 sum of squares reduced in a fixed butterfly order.
+template <bool OUT_BF16>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int64_t ldx,
+                                                      const int32_t* __restrict__ rows,
+                                                      int64_t n_rows, const float* __restrict__ g,
+                                                      int d, float eps, void* __restrict__ y,
+                                                      int64_t ldy) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (r >= n_rows) return;
+    const int64_t src = rows ? (int64_t)rows[r] : r;
+    const float4* xr = reinterpret_cast<const float4*>(x + src * ldx);
+    const float4* g4 = reinterpret_cast<const float4*>(g);
+    float ss = 0.f;
+    for (int c = lane; c < d / 4; c += 64) {
+        const float4 v = xr[c];
+        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+    ss = wave_sum(ss);
+    const float sc = rsqrtf(ss / (float)d + eps);
+    for (int c = lane; c < d / 4; c += 64) {
+        const float4 v = xr[c];
+        const float4 w = g4[c];
+        const float a = v.x * sc * w.x, b = v.y * sc * w.y, e = v.z * sc * w.z, f = v.w * sc * w.w;
+        if constexpr (OUT_BF16) {
+            uint2 o;
+            o.x = pack_bf16x2(a, b);
+            o.y = pack_bf16x2(e, f);
+            reinterpret_cast<uint2*>(static_cast<uint16_t*>(y) + r * ldy)[c] = o;
+        } else {
+            reinterpret_cast<float4*>(static_cast<float*>(y) + r * ldy)[c] = make_float4(a, b, e, f);
+        }
+    }
+}
+
+// ---------------------------------------------------------------- RoPE
+// One thread per rotated pair (token, head, i < hd/2): dims i and i + hd/2 rotate by
+// theta = pos * base^(-2i/hd), whose cos/sin come from the float32 table cs[pos][i].
+template <bool BF16>
+__global__ __launch_bounds__(256) void rope_kernel(void* __restrict__ qkv, int64_t ld, int64_t T,
+                                                   const int32_t* __restrict__ pos, int n_heads,
+                                                   int hd, const float2* __restrict__ cs) {
+    const int half = hd >> 1;
+    const int64_t per_tok = (int64_t)n_heads * half;
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= T * per_tok) return;
+    const int64_t t = idx / per_tok;
+    const int rem = (int)(idx - t * per_tok);
+    const int h = rem / half, i = rem - (rem / half) * half;
+    const float2 c = cs[(int64_t)pos[t] * half + i];
+    const int64_t e1 = t * ld + (int64_t)h * hd + i, e2 = e1 + half;
+    if constexpr (BF16) {
+        uint16_t* p = static_cast<uint16_t*>(qkv);
+        const float x1 = bf16_to_f32(p[e1]), x2 = bf16_to_f32(p[e2]);
+        p[e1] = (uint16_t)f32_to_bf16(x1 * c.x - x2 * c.y);
+        p[e2] = (uint16_t)f32_to_bf16(x2 * c.x + x1 * c.y);
+    } else {
+        float* p = static_cast<float*>(qkv);
+        const float x1 = p[e1], x2 = p[e2];
+        p[e1] = x1 * c.x - x2 * c.y;
+        p[e2] = x2 * c.x + x1 * c.y;
+    }
+}
+
+// ---------------------------------------------------------------- fp32 SwiGLU
+__global__ __launch_bounds__(256) void swiglu_f32_kernel(const float* __restrict__ gu,
+                                                         float* __restrict__ u, int64_t T,
+                                                         int d_ff) {
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= T * d_ff) return;
+    const int64_t t = idx / d_ff;
+    const int j = (int)(idx - t * d_ff);
+    const float* row = gu + t * 2 * (int64_t)d_ff + (j >> 5) * 64 + (j & 31);
+    const float gv = row[0], uv = row[32];
+    u[idx] = gv / (1.f + expf(-gv)) * uv;
+}
+
+// ---------------------------------------------------------------- row gather
+__global__ __launch_bounds__(256) void gather_rows_kernel(const uint32_t* __restrict__ src,
+                                                          int64_t ld_src,
+                                                          const int32_t* __restrict__ rows,
+                                                          int words,
+                                                          uint32_t* __restrict__ dst,
+                                                          int64_t ld_dst) {
+    const int64_t r = blockIdx.x;
+    const uint32_t* s = src + (int64_t)rows[r] * ld_src;
+    uint32_t* o = dst + r * ld_dst;
+    for (int c = threadIdx.x; c < words; c += 256) o[c] = s[c];
+}
+
+// ---------------------------------------------------------------- LSE + verdicts
+// One workgroup per prompt.  LSE = max + log(sum exp(z - max)) over the full vocabulary
+// (fixed-order reductions), lp_v = z[vid_v] - LSE, then p = softmax(lp), q = max p and
+// the first argmax.
+__global__ __launch_bounds__(256) void lse_verdict_kernel(const float* __restrict__ logits,
+                                                          int64_t ld, int V,
+                                                          const int32_t* __restrict__ vid, int nv,
+                                                          float* __restrict__ lp,
+                                                          float* __restrict__ probs,
+                                                          float* __restrict__ conf,
+                                                          int32_t* __restrict__ verdict) {
+    __shared__ float red[4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int b = blockIdx.x;
+    const float* z = logits + (int64_t)b * ld;
+    float mx = -INFINITY;
+    for (int i = tid; i < V; i += 256) mx = fmaxf(mx, z[i]);
+    mx = wave_max(mx);
+    if (lane == 0) red[wave] = mx;
+    __syncthreads();
+    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    __syncthreads();
+    float s = 0.f;
+    for (int i = tid; i < V; i += 256) s += expf(z[i] - mx);
+    s = wave_sum(s);
+    if (lane == 0) red[wave] = s;
+    __syncthreads();
+    if (tid == 0) {
+        const float lse = mx + logf(((red[0] + red[1]) + red[2]) + red[3]);
+        float l[16];
+        float m2 = -INFINITY;
+        for (int v = 0; v < nv; ++v) {
+            l[v] = z[vid[v]] - lse;
+            lp[b * nv + v] = l[v];
+            m2 = fmaxf(m2, l[v]);
+        }
+        float se = 0.f;
+        for (int v = 0; v < nv; ++v) {
+            l[v] = expf(l[v] - m2);
+            se += l[v];
+        }
+        int best = 0;
+        float q = -1.f;
+        for (int v = 0; v < nv; ++v) {
+            const float p = l[v] / se;
+            if (probs) probs[b * nv + v] = p;
+            if (p > q) {
+                q = p;
+                best = v;
+            }
+        }
+        conf[b] = q;
+        if (verdict) verdict[b] = best;
+    }
+}
+
+// ---------------------------------------------------------------- selection
+// flags[i] = 1 if candidate i is deferred.  Threshold: !(q_i >= tau).  Budget: the rank
+// of i in the order (NaN first, confidence ascending, index ascending) is below k.
+__global__ __launch_bounds__(256) void select_flags_kernel(const float* __restrict__ q, int n,
+                                                           int mode, float tau, int k,
+                                                           int32_t* __restrict__ flags) {
+    __shared__ float keys[256];
+    const int tid = threadIdx.x;
+    const int i = blockIdx.x * 256 + tid;
+    const float qi = i < n ? q[i] : 0.f;
+    if (mode == 0) {
+        if (i < n) flags[i] = !(qi >= tau);
+        return;
+    }
+    const float ki = __builtin_isnan(qi) ? -INFINITY : qi;
+    int rank = 0;
+    for (int j0 = 0; j0 < n; j0 += 256) {
+        __syncthreads();
+        const int j = j0 + tid;
+        const float qj = j < n ? q[j] : 0.f;
+        keys[tid] = __builtin_isnan(qj) ? -INFINITY : qj;
+        __syncthreads();
+        const int lim = min(256, n - j0);
+        for (int jj = 0; jj < lim; ++jj) {
+            const float kj = keys[jj];
+            rank += (kj < ki) || (kj == ki && j0 + jj < i);
+        }
+    }
+    if (i < n) flags[i] = rank < k;
+}
+
+// Ordered compaction in one workgroup: ballot + popcount prefix per wave, wave totals
+// through LDS, carried across 1024-element chunks.  flags may alias defer_idx: every
+// chunk reads its flags before any thread writes, and writes never pass the chunk.
+__global__ __launch_bounds__(1024) void select_compact_kernel(const int32_t* flags, int n,
+                                                              int32_t* defer_idx,
+                                                              int32_t* __restrict__ accept_idx,
+                                                              int32_t* __restrict__ counts) {
+    __shared__ int wsum[16];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int carry = 0;
+    for (int i0 = 0; i0 < n; i0 += 1024) {
+        const int i = i0 + tid;
+        const int f = i < n ? flags[i] : 0;
+        const uint64_t m = __ballot(f != 0);
+        const int pre = __popcll(m & ((1ull << lane) - 1ull));
+        if (lane == 0) wsum[wave] = __popcll(m);
+        __syncthreads();
+        int wpre = 0, tot = 0;
+        for (int w = 0; w < 16; ++w) {
+            wpre += w < wave ? wsum[w] : 0;
+            tot += wsum[w];
+        }
+        const int before = carry + wpre + pre;  // deferred candidates with index < i
+        if (i < n) {
+            if (f) defer_idx[before] = i;
+            else accept_idx[i - before] = i;
+        }
+        carry += tot;
+        __syncthreads();
+    }
+    if (tid == 0) {
+        counts[0] = carry;
+        counts[1] = n - carry;
+    }
+}
+
+inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+hipError_t launch_embed(Act wt, const int32_t* tokens, int64_t row_stride, const int32_t* cu,
+                        int B, int64_t T, const void* embed, int d, int vocab, float* x,
+                        int32_t* pos, int32_t* err_flag, hipStream_t s) {
+    if (wt == Act::BF16)
+        embed_kernel<true><<<blocks_for(T, 4), 256, 0, s>>>(tokens, row_stride, cu, B, T, embed,
+                                                            d, vocab, x, pos, err_flag);
+    else
+        embed_kernel<false><<<blocks_for(T, 4), 256, 0, s>>>(tokens, row_stride, cu, B, T, embed,
+                                                             d, vocab, x, pos, err_flag);
+    return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(Act out, const float* x, int64_t ldx, const int32_t* rows,
+                          int64_t n_rows, const float* g, int d, float eps, void* y, int64_t ldy,
+                          hipStream_t s) {
+    if (n_rows == 0) return hipSuccess;
+    if (out == Act::BF16)
+        rmsnorm_kernel<true><<<blocks_for(n_rows, 4), 256, 0, s>>>(x, ldx, rows, n_rows, g, d,
+                                                                   eps, y, ldy);
+    else
+        rmsnorm_kernel<false><<<blocks_for(n_rows, 4), 256, 0, s>>>(x, ldx, rows, n_rows, g, d,
+                                                                    eps, y, ldy);
+    return hipGetLastError();
+}
+
+hipError_t launch_rope(Act t, void* qkv, int64_t ld, int64_t T, const int32_t* pos, int n_heads,
+                       int head_dim, const float2* cs, hipStream_t s) {
+    const int64_t n = T * n_heads * (head_dim / 2);
+    if (n == 0) return hipSuccess;
+    if (t == Act::BF16)
+        rope_kernel<true><<<blocks_for(n, 256), 256, 0, s>>>(qkv, ld, T, pos, n_heads, head_dim, cs);
+    else
+        rope_kernel<false><<<blocks_for(n, 256), 256, 0, s>>>(qkv, ld, T, pos, n_heads, head_dim, cs);
+    return hipGetLastError();
+}
+
+hipError_t launch_swiglu_f32(const float* gu, float* u, int64_t T, int d_ff, hipStream_t s) {
+    const int64_t n = T * d_ff;
+    if (n == 0) return hipSuccess;
+    swiglu_f32_kernel<<<blocks_for(n, 256), 256, 0, s>>>(gu, u, T, d_ff);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const void* src, int64_t ld_src, const int32_t* rows, int64_t n,
+                              int cols, int elem_bytes, void* dst, int64_t ld_dst, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    // rows are moved as 4-byte words: cols * elem_bytes and the leading dimensions (in
+    // bytes) are multiples of 4 for every caller (even bf16 widths).
+    const int words = cols * elem_bytes / 4;
+    gather_rows_kernel<<<(unsigned)n, 256, 0, s>>>(static_cast<const uint32_t*>(src),
+                                                   ld_src * elem_bytes / 4, rows, words,
+                                                   static_cast<uint32_t*>(dst),
+                                                   ld_dst * elem_bytes / 4);
+    return hipGetLastError();
+}
+
+hipError_t launch_lse_verdict(const float* logits, int64_t ld, int B, int V, const int32_t* vid,
+                              int nv, float* lp, float* probs, float* conf, int32_t* verdict,
+                              hipStream_t s) {
+    lse_verdict_kernel<<<B, 256, 0, s>>>(logits, ld, V, vid, nv, lp, probs, conf, verdict);
+    return hipGetLastError();
+}
+
+hipError_t launch_select(const float* conf, int n, int mode, float tau, int k, int32_t* flags,
+                         int32_t* defer_idx, int32_t* accept_idx, int32_t* counts,
+                         hipStream_t s) {
+    select_flags_kernel<<<blocks_for(n, 256), 256, 0, s>>>(conf, n, mode, tau, k, flags);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    select_compact_kernel<<<1, 1024, 0, s>>>(flags, n, defer_idx, accept_idx, counts);
+    return hipGetLastError();
+}
+
+}  // namespace surr

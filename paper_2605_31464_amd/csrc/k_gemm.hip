@@ -1,0 +1,287 @@
+// Projection GEMMs C = A[M,K] * B[N,K]^T with fused epilogues.
+//
+// bf16 path: v_mfma_f32_32x32x16_bf16 on a BM x BN workgroup tile (4 wavefronts, each
+// WM x WN), K in steps of 64.  Both operands are K-contiguous, so one 16-byte chunk of
+// a row is exactly the 8 consecutive k values an MFMA lane supplies.  Tiles go
+// global -> registers -> LDS (double buffered, one barrier per K step); LDS rows hold
+// 8 chunks whose order is XOR-swizzled by the row to spread the 16-byte reads over the
+// banks.  The MFMA is issued with the weight fragment as its A operand and the
+// activation fragment as its B operand, so each lane ends up owning one output row m
+// and runs of 4 consecutive output columns n - the shape the epilogues want (8- or
+// 16-byte stores, gate/up pairs and residual rows in one lane).
+//
+// fp32 path: a plain LDS-tiled FMA kernel for the float32 model.
+#include "common.h"
+#include "kernels.h"
+
+namespace surr {
+namespace {
+
+constexpr int kBK = 64;
+
+template <int BM, int BN, int WM, int WN>
+struct Tile {
+    static constexpr int WAVES_N = BN / WN;
+    static_assert((BM / WM) * (BN / WN) == 4, "four wavefronts per workgroup");
+    static constexpr int FM = WM / 32, FN = WN / 32;
+    static constexpr int A_LD = BM * 8 / 256;  // 16-byte chunks per thread per K step
+    static constexpr int B_LD = BN * 8 / 256;
+    static constexpr int STAGE = (BM + BN) * 8;  // uint4 slots per LDS stage
+};
+
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+
+__device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); }
+
+template <int BM, int BN, int WM, int WN, Epi EPI>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restrict__ A,
+                                                        int64_t lda,
+                                                        const uint16_t* __restrict__ B,
+                                                        int64_t ldb, void* __restrict__ C,
+                                                        int64_t ldc, int M, int N, int K) {
+    using S = Tile<BM, BN, WM, WN>;
+    __shared__ uint4 lds[2 * S::STAGE];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / S::WAVES_N, wn = wave % S::WAVES_N;
+
+    // Grouped tile order: GROUP consecutive M tiles sweep N together so the A rows they
+    // share stay in L2.
+    constexpr int GROUP = 8;
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    const int pid = blockIdx.x;
+    const int width = GROUP * tiles_n;
+    const int first_m = (pid / width) * GROUP;
+    const int gsz = min(tiles_m - first_m, GROUP);
+    const int tm = first_m + (pid % width) % gsz;
+    const int tn = (pid % width) / gsz;
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    // Thread tid moves chunk (tid & 7) of rows (tid >> 3) + 32 i.  Rows past M or N are
+    // clamped to the last valid row (their results are never stored).
+    const int c = tid & 7;
+    const uint16_t* a_src[S::A_LD];
+    const uint16_t* b_src[S::B_LD];
+    int a_dst[S::A_LD], b_dst[S::B_LD];
+#pragma unroll
+    for (int i = 0; i < S::A_LD; ++i) {
+        const int r = (tid >> 3) + 32 * i;
+        a_src[i] = A + (int64_t)min(m0 + r, M - 1) * lda + c * 8;
+        a_dst[i] = r * 8 + (c ^ swz(r));
+    }
+#pragma unroll
+    for (int i = 0; i < S::B_LD; ++i) {
+        const int r = (tid >> 3) + 32 * i;
+        b_src[i] = B + (int64_t)min(n0 + r, N - 1) * ldb + c * 8;
+        b_dst[i] = (BM + r) * 8 + (c ^ swz(r));
+    }
+    uint4 ra[S::A_LD], rb[S::B_LD];
+
+    f32x16 acc[S::FM][S::FN];
+#pragma unroll
+    for (int i = 0; i < S::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < S::FN; ++j) acc[i][j] = f32x16{};
+
+    const int nk = K / kBK;
+#pragma unroll
+    for (int i = 0; i < S::A_LD; ++i) ra[i] = *reinterpret_cast<const uint4*>(a_src[i]);
+#pragma unroll
+    for (int i = 0; i < S::B_LD; ++i) rb[i] = *reinterpret_cast<const uint4*>(b_src[i]);
+#pragma unroll
+    for (int i = 0; i < S::A_LD; ++i) lds[a_dst[i]] = ra[i];
+#pragma unroll
+    for (int i = 0; i < S::B_LD; ++i) lds[b_dst[i]] = rb[i];
+    __syncthreads();
+
+    for (int kt = 0; kt < nk; ++kt) {
+        const int st = kt & 1;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            const int k0 = (kt + 1) * kBK;
+#pragma unroll
+            for (int i = 0; i < S::A_LD; ++i) ra[i] = *reinterpret_cast<const uint4*>(a_src[i] + k0);
+#pragma unroll
+            for (int i = 0; i < S::B_LD; ++i) rb[i] = *reinterpret_cast<const uint4*>(b_src[i] + k0);
+        }
+        const uint4* L = lds + st * S::STAGE;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const int chunk = 2 * s + (lane >> 5);
+            bf16x8 af[S::FM], bw[S::FN];
+#pragma unroll
+            for (int i = 0; i < S::FM; ++i) {
+                const int r = wm * WM + i * 32 + (lane & 31);
+                af[i] = __builtin_bit_cast(bf16x8, L[r * 8 + (chunk ^ swz(r))]);
+            }
+#pragma unroll
+            for (int j = 0; j < S::FN; ++j) {
+                const int r = wn * WN + j * 32 + (lane & 31);
+                bw[j] = __builtin_bit_cast(bf16x8, L[(BM + r) * 8 + (chunk ^ swz(r))]);
+            }
+#pragma unroll
+            for (int i = 0; i < S::FM; ++i)
+#pragma unroll
+                for (int j = 0; j < S::FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw[j], af[i], acc[i][j],
+                                                                        0, 0, 0);
+        }
+        if (more) {
+            uint4* Ln = lds + (st ^ 1) * S::STAGE;
+#pragma unroll
+            for (int i = 0; i < S::A_LD; ++i) Ln[a_dst[i]] = ra[i];
+#pragma unroll
+            for (int i = 0; i < S::B_LD; ++i) Ln[b_dst[i]] = rb[i];
+        }
+        __syncthreads();
+    }
+
+    // Lane owns row m = m0 + wm*WM + 32 i + (lane & 31) and, per 32-column fragment j,
+    // columns nb + 8 q + 4 (lane >> 5) + {0..3} in acc[i][j][4 q + {0..3}].
+    const int h = lane >> 5;
+#pragma unroll
+    for (int i = 0; i < S::FM; ++i) {
+        const int m = m0 + wm * WM + i * 32 + (lane & 31);
+        if (m >= M) continue;
+        if constexpr (EPI == Epi::SwiGLU) {
+            // Fragment pairs (2p, 2p+1) hold gate and up rows of the same 32 outputs.
+#pragma unroll
+            for (int j = 0; j < S::FN; j += 2) {
+                const int nb = n0 + wn * WN + j * 32;
+                if (nb >= N) continue;
+                uint16_t* out = static_cast<uint16_t*>(C) + (int64_t)m * ldc + nb / 2;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    float v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        v[e] = silu(acc[i][j][4 * q + e]) * acc[i][j + 1][4 * q + e];
+                    uint2 o;
+                    o.x = pack_bf16x2(v[0], v[1]);
+                    o.y = pack_bf16x2(v[2], v[3]);
+                    *reinterpret_cast<uint2*>(out + 8 * q + 4 * h) = o;
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < S::FN; ++j) {
+                const int nb = n0 + wn * WN + j * 32;
+                if (nb >= N) continue;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int n = nb + 8 * q + 4 * h;
+                    const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                     acc[i][j][4 * q + 3]};
+                    if constexpr (EPI == Epi::StoreAct) {
+                        uint2 o;
+                        o.x = pack_bf16x2(v[0], v[1]);
+                        o.y = pack_bf16x2(v[2], v[3]);
+                        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(C) + (int64_t)m * ldc + n) = o;
+                    } else if constexpr (EPI == Epi::StoreF32) {
+                        *reinterpret_cast<f32x4*>(static_cast<float*>(C) + (int64_t)m * ldc + n) = v;
+                    } else {
+                        f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(C) + (int64_t)m * ldc + n);
+                        *p = *p + v;
+                    }
+                }
+            }
+        }
+    }
+}
+
+template <int BM, int BN, int WM, int WN, Epi EPI>
+hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
+                    int M, int N, int K, hipStream_t s) {
+    const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    gemm_bf16_kernel<BM, BN, WM, WN, EPI><<<(unsigned)tiles, 256, 0, s>>>(
+        static_cast<const uint16_t*>(A), lda, static_cast<const uint16_t*>(B), ldb, C, ldc, M, N, K);
+    return hipGetLastError();
+}
+
+template <Epi EPI>
+hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
+                         int64_t ldc, int M, int N, int K, hipStream_t s) {
+    if (M <= 128) return run_bf16<128, 128, 64, 64, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
+    return run_bf16<256, 256, 128, 128, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
+}
+
+// ---------------------------------------------------------------- fp32 FMA GEMM
+template <Epi EPI>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, int64_t lda,
+                                                       const float* __restrict__ B, int64_t ldb,
+                                                       float* __restrict__ C, int64_t ldc, int M,
+                                                       int N, int K) {
+    __shared__ float As[16][68];
+    __shared__ float Bs[16][68];
+    const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+    const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+    float acc[4][4] = {};
+    for (int k0 = 0; k0 < K; k0 += 16) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int idx = tid + 256 * e, r = idx >> 4, kk = idx & 15;
+            As[kk][r] = A[(int64_t)min(m0 + r, M - 1) * lda + k0 + kk];
+            Bs[kk][r] = B[(int64_t)min(n0 + r, N - 1) * ldb + k0 + kk];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < 16; ++kk) {
+            float a[4], b[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+    const int n = n0 + tx * 4;
+    if (n >= N) return;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int m = m0 + ty * 4 + i;
+        if (m >= M) continue;
+        float* p = C + (int64_t)m * ldc + n;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (EPI == Epi::ResidAddF32) p[j] += acc[i][j];
+            else p[j] = acc[i][j];
+        }
+    }
+}
+
+template <Epi EPI>
+hipError_t run_f32(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
+                   int M, int N, int K, hipStream_t s) {
+    dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64));
+    gemm_f32_kernel<EPI><<<grid, 256, 0, s>>>(static_cast<const float*>(A), lda,
+                                               static_cast<const float*>(B), ldb,
+                                               static_cast<float*>(C), ldc, M, N, K);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, int64_t ldb,
+                       void* C, int64_t ldc, int M, int N, int K, hipStream_t s) {
+    if (M <= 0 || N <= 0) return hipSuccess;
+    if (t == Act::F32) {
+        switch (e) {
+            case Epi::ResidAddF32: return run_f32<Epi::ResidAddF32>(A, lda, B, ldb, C, ldc, M, N, K, s);
+            case Epi::StoreAct:
+            case Epi::StoreF32: return run_f32<Epi::StoreF32>(A, lda, B, ldb, C, ldc, M, N, K, s);
+            default: return hipErrorInvalidValue;  // fp32 SwiGLU runs as its own kernel
+        }
+    }
+    switch (e) {
+        case Epi::StoreAct: return dispatch_bf16<Epi::StoreAct>(A, lda, B, ldb, C, ldc, M, N, K, s);
+        case Epi::ResidAddF32: return dispatch_bf16<Epi::ResidAddF32>(A, lda, B, ldb, C, ldc, M, N, K, s);
+        case Epi::SwiGLU: return dispatch_bf16<Epi::SwiGLU>(A, lda, B, ldb, C, ldc, M, N, K, s);
+        case Epi::StoreF32: return dispatch_bf16<Epi::StoreF32>(A, lda, B, ldb, C, ldc, M, N, K, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace surr

@@ -1,0 +1,67 @@
+// Host-side launchers of the gfx950 kernels (one translation unit per kernel family).
+// Every launcher enqueues on `stream` and returns the hipError_t of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace surr {
+
+enum class Act { F32, BF16 };  // storage type of activations and matrices
+
+// ---- k_elementwise.hip
+// Gather embedding rows of the packed tokens into the fp32 residual x[T, d] and
+// record each token's position inside its prompt.  cu[B+1] are prompt offsets.
+hipError_t launch_embed(Act wt, const int32_t* tokens, int64_t row_stride, const int32_t* cu,
+                        int B, int64_t T, const void* embed, int d, int vocab, float* x,
+                        int32_t* pos, int32_t* err_flag, hipStream_t s);
+
+// y[r] = x[rows ? rows[r] : r] * rsqrt(mean(x^2) + eps) * g, stored as `out` type.
+hipError_t launch_rmsnorm(Act out, const float* x, int64_t ldx, const int32_t* rows,
+                          int64_t n_rows, const float* g, int d, float eps, void* y, int64_t ldy,
+                          hipStream_t s);
+
+// In-place rotate-half RoPE on the first n_heads heads of each row of qkv.
+hipError_t launch_rope(Act t, void* qkv, int64_t ld, int64_t T, const int32_t* pos, int n_heads,
+                       int head_dim, const float2* cs, hipStream_t s);
+
+// u[t, j] = silu(gu[t, gate(j)]) * gu[t, up(j)] with gate/up interleaved in 32-column
+// blocks (fp32 path; the bf16 path fuses this into the GEMM epilogue).
+hipError_t launch_swiglu_f32(const float* gu, float* u, int64_t T, int d_ff, hipStream_t s);
+
+// Copy rows rows[r] of src into dst row r (elem_bytes per element).
+hipError_t launch_gather_rows(const void* src, int64_t ld_src, const int32_t* rows, int64_t n,
+                              int cols, int elem_bytes, void* dst, int64_t ld_dst, hipStream_t s);
+
+// Per prompt b: full-vocab log-softmax of logits[b] at the verdict ids, then the
+// renormalised verdict distribution, its max and first argmax.
+hipError_t launch_lse_verdict(const float* logits, int64_t ld, int B, int V, const int32_t* vid,
+                              int nv, float* lp, float* probs, float* conf, int32_t* verdict,
+                              hipStream_t s);
+
+// Selection: flags then ordered compaction.
+hipError_t launch_select(const float* conf, int n, int mode, float tau, int k, int32_t* flags,
+                         int32_t* defer_idx, int32_t* accept_idx, int32_t* counts,
+                         hipStream_t s);
+
+// ---- k_gemm.hip
+enum class Epi { StoreAct, ResidAddF32, SwiGLU, StoreF32 };
+
+// C = A[M,K] * B[N,K]^T (both K-contiguous), fp32 accumulation, fused epilogue:
+//   StoreAct    C (activation type) [M, N]
+//   ResidAddF32 C (fp32) += result
+//   SwiGLU      B rows interleave gate/up in 32-row blocks; C[M, N/2] = silu(g) * u
+//   StoreF32    C (fp32) [M, N]
+hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, int64_t ldb,
+                       void* C, int64_t ldc, int M, int N, int K, hipStream_t s);
+
+// ---- k_attention.hip
+// Causal GQA attention over the packed qkv rows.  work[i] = (prompt, q_tile) items;
+// grid = n_items * n_q_heads.  q_tile covers rows [q_tile * 128, +128) of the prompt
+// (64 rows for the fp32 kernel).
+hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, void* out, int64_t ld_out,
+                            const int32_t* cu, const int2* work, int n_items, int n_q_heads,
+                            int n_kv_heads, int head_dim, hipStream_t s);
+int attention_q_tile(Act t);
+
+}  // namespace surr

@@ -1,0 +1,542 @@
+// Host runtime behind the C ABI of include/surrogate.h: argument checks, the device
+// weight arena (re-laid out for the kernels), the per-call planner and the launch
+// sequence of one prefill-only scoring pass.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "surrogate.h"
+
+using surr::Act;
+using surr::Epi;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+surrogate_status fail(surrogate_status s, const std::string& msg) {
+    g_last_error = msg;
+    return s;
+}
+
+#define SURR_HIP(expr)                                                                      \
+    do {                                                                                    \
+        hipError_t e_ = (expr);                                                             \
+        if (e_ != hipSuccess)                                                               \
+            return fail(SURR_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));     \
+    } while (0)
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct LayerW {
+    float* attn_norm;
+    void* w_qkv;  // [d_q + 2 d_kv, d]: q heads, k heads, v heads
+    void* w_o;
+    float* mlp_norm;
+    void* w_gu;  // [2 d_ff, d]: 32-row blocks alternate gate rows and up rows
+    void* w_down;
+};
+
+// Byte offsets of one call's workspace regions.
+struct WsLayout {
+    size_t cu, last, vid, work, work_last, pos, x, h, qkv, o, u, gu, o_last, x_last, h_last,
+        u_last, gu_last, y, logits, total;
+};
+
+bool valid_config(const surrogate_config* c, std::string* why) {
+    auto bad = [&](const char* m) { *why = m; return false; };
+    if (c->dtype != SURR_F32 && c->dtype != SURR_BF16) return bad("dtype must be SURR_F32 or SURR_BF16");
+    if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 ||
+        c->d_ff < 1 || c->vocab < 1 || c->max_pos < 1)
+        return bad("sizes must be positive");
+    if (c->n_q_heads % c->n_kv_heads) return bad("n_q_heads must be a multiple of n_kv_heads");
+    if (!(c->rope_base > 0.f) || !(c->rms_eps >= 0.f)) return bad("rope_base > 0 and rms_eps >= 0 required");
+    const int64_t dq = (int64_t)c->n_q_heads * c->head_dim;
+    if (c->dtype == SURR_BF16) {
+        if (c->head_dim != 64 && c->head_dim != 128) return bad("bf16 needs head_dim 64 or 128");
+        if (c->d_model % 64 || dq % 64 || c->d_ff % 64) return bad("bf16 needs d_model, d_q, d_ff multiples of 64");
+    } else {
+        if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
+            return bad("f32 needs head_dim 32, 64 or 128");
+        if (c->d_model % 32 || dq % 32 || c->d_ff % 32) return bad("f32 needs d_model, d_q, d_ff multiples of 32");
+    }
+    if (c->vocab % 32) return bad("vocab must be a multiple of 32");
+    if ((int64_t)c->max_pos * c->vocab <= 0) return bad("overflow");
+    return true;
+}
+
+void tensor_shape(const surrogate_config* c, int idx, int64_t* rows, int64_t* cols, int32_t* dt) {
+    const int64_t d = c->d_model, dq = (int64_t)c->n_q_heads * c->head_dim,
+                  dkv = (int64_t)c->n_kv_heads * c->head_dim, ff = c->d_ff, V = c->vocab;
+    const int last = 1 + 9 * c->n_layers;
+    *dt = c->dtype;
+    if (idx == 0 || idx == last + 1) { *rows = V; *cols = d; return; }
+    if (idx == last) { *rows = 1; *cols = d; *dt = SURR_F32; return; }
+    switch ((idx - 1) % 9) {
+        case 0: case 5: *rows = 1; *cols = d; *dt = SURR_F32; return;
+        case 1: *rows = dq; *cols = d; return;
+        case 2: case 3: *rows = dkv; *cols = d; return;
+        case 4: *rows = d; *cols = dq; return;
+        case 6: case 7: *rows = ff; *cols = d; return;
+        default: *rows = d; *cols = ff; return;
+    }
+}
+
+}  // namespace
+
+struct surrogate_model {
+    surrogate_config cfg{};
+    Act act = Act::BF16;
+    size_t esz = 2;
+    char* arena = nullptr;
+    void* embed = nullptr;
+    void* lm_head = nullptr;
+    float* final_norm = nullptr;
+    std::vector<LayerW> layers;
+    float2* rope_cs = nullptr;
+    int32_t* err_flag = nullptr;
+    std::mutex mu;  // guards the pinned staging buffer
+    void* pinned = nullptr;
+    size_t pinned_bytes = 0;
+    hipEvent_t staged = nullptr;
+    bool staged_pending = false;
+    // measurement hook
+    bool profiling = false;
+    std::vector<hipEvent_t> ev_pool;          // events owned by the model
+    std::vector<std::pair<int, size_t>> rec;  // (phase, index of the start event)
+    size_t ev_used = 0;
+
+    int64_t d_q() const { return (int64_t)cfg.n_q_heads * cfg.head_dim; }
+    int64_t d_kv() const { return (int64_t)cfg.n_kv_heads * cfg.head_dim; }
+    int64_t d_qkv() const { return d_q() + 2 * d_kv(); }
+};
+
+namespace {
+
+WsLayout layout(const surrogate_model* m, int64_t B, int64_t T) {
+    const surrogate_config& c = m->cfg;
+    const int64_t qt = surr::attention_q_tile(m->act);
+    const int64_t items = (T + qt - 1) / qt + B;
+    const size_t e = m->esz;
+    const bool f32 = m->act == Act::F32;
+    WsLayout w{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
+    w.cu = take(4 * (B + 1));
+    w.last = take(4 * B);
+    w.vid = take(4 * 16);
+    w.work = take(8 * items);
+    w.work_last = take(8 * B);
+    w.pos = take(4 * T);
+    w.x = take(4 * T * c.d_model);
+    w.h = take(e * T * c.d_model);
+    w.qkv = take(e * T * m->d_qkv());
+    w.o = take(e * T * m->d_q());
+    w.u = take(e * T * c.d_ff);
+    w.gu = f32 ? take(4 * T * 2 * c.d_ff) : 0;
+    w.o_last = take(e * B * m->d_q());
+    w.x_last = take(4 * B * c.d_model);
+    w.h_last = take(e * B * c.d_model);
+    w.u_last = take(e * B * c.d_ff);
+    w.gu_last = f32 ? take(4 * B * 2 * c.d_ff) : 0;
+    w.y = take(e * B * c.d_model);
+    w.logits = take(4 * B * c.vocab);
+    w.total = off;
+    return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+surrogate_status surrogate_tensor_count(const surrogate_config* cfg, int32_t* n_out) {
+    if (!cfg || !n_out) return fail(SURR_E_INVALID_ARG, "null argument");
+    if (cfg->n_layers < 1) return fail(SURR_E_SHAPE, "n_layers must be >= 1");
+    *n_out = 3 + 9 * cfg->n_layers;
+    return SURR_OK;
+}
+
+surrogate_status surrogate_tensor_shape(const surrogate_config* cfg, int32_t index, int64_t* rows,
+                                        int64_t* cols, int32_t* dtype_out) {
+    if (!cfg || !rows || !cols || !dtype_out) return fail(SURR_E_INVALID_ARG, "null argument");
+    std::string why;
+    if (!valid_config(cfg, &why)) return fail(SURR_E_SHAPE, why);
+    if (index < 0 || index >= 3 + 9 * cfg->n_layers) return fail(SURR_E_INVALID_ARG, "tensor index out of range");
+    tensor_shape(cfg, index, rows, cols, dtype_out);
+    return SURR_OK;
+}
+
+void surrogate_free(surrogate_model* m) {
+    if (!m) return;
+    for (hipEvent_t e : m->ev_pool) hipEventDestroy(e);
+    if (m->staged) {
+        hipEventSynchronize(m->staged);
+        hipEventDestroy(m->staged);
+    }
+    if (m->pinned) hipHostFree(m->pinned);
+    if (m->arena) hipFree(m->arena);
+    delete m;
+}
+
+surrogate_status surrogate_load_weights(const surrogate_config* cfg, const void* const* tensors,
+                                        int32_t n_tensors, int32_t tensors_on_device,
+                                        hipStream_t stream, surrogate_model** out) {
+    if (!cfg || !tensors || !out) return fail(SURR_E_INVALID_ARG, "null argument");
+    *out = nullptr;
+    std::string why;
+    if (!valid_config(cfg, &why)) return fail(SURR_E_SHAPE, why);
+    const int32_t want = 3 + 9 * cfg->n_layers;
+    if (n_tensors != want)
+        return fail(SURR_E_WEIGHTS, "expected " + std::to_string(want) + " tensors, got " + std::to_string(n_tensors));
+    for (int i = 0; i < n_tensors; ++i)
+        if (!tensors[i]) return fail(SURR_E_INVALID_ARG, "tensor " + std::to_string(i) + " is null");
+
+    surrogate_model* m = new surrogate_model();
+    m->cfg = *cfg;
+    m->act = cfg->dtype == SURR_BF16 ? Act::BF16 : Act::F32;
+    m->esz = cfg->dtype == SURR_BF16 ? 2 : 4;
+    const surrogate_config& c = m->cfg;
+    const size_t e = m->esz, d = c.d_model, ff = c.d_ff, V = c.vocab;
+    const size_t dq = m->d_q(), dkv = m->d_kv(), half = c.head_dim / 2;
+
+    // Arena: embed, layers, final norm, head, RoPE table, error word.
+    size_t off = 0;
+    auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
+    const size_t o_embed = take(V * d * e);
+    struct LOff { size_t an, qkv, o, mn, gu, dn; };
+    std::vector<LOff> lo(c.n_layers);
+    for (auto& l : lo) {
+        l.an = take(4 * d);
+        l.qkv = take((dq + 2 * dkv) * d * e);
+        l.o = take(d * dq * e);
+        l.mn = take(4 * d);
+        l.gu = take(2 * ff * d * e);
+        l.dn = take(d * ff * e);
+    }
+    const size_t o_fn = take(4 * d), o_head = take(V * d * e);
+    const size_t o_rope = take((size_t)c.max_pos * half * sizeof(float2)), o_err = take(4);
+    if (hipMalloc(&m->arena, off) != hipSuccess) {
+        surrogate_free(m);
+        return fail(SURR_E_OOM, "weight arena of " + std::to_string(off) + " bytes");
+    }
+    char* A = m->arena;
+    m->embed = A + o_embed;
+    m->final_norm = reinterpret_cast<float*>(A + o_fn);
+    m->lm_head = A + o_head;
+    m->rope_cs = reinterpret_cast<float2*>(A + o_rope);
+    m->err_flag = reinterpret_cast<int32_t*>(A + o_err);
+    for (auto& l : lo)
+        m->layers.push_back({reinterpret_cast<float*>(A + l.an), A + l.qkv, A + l.o,
+                             reinterpret_cast<float*>(A + l.mn), A + l.gu, A + l.dn});
+
+    const hipMemcpyKind kind = tensors_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+    std::vector<float2> cs((size_t)c.max_pos * half);
+    auto body = [&]() -> surrogate_status {
+        auto cp = [&](void* dst, const void* src, size_t bytes) {
+            return hipMemcpyAsync(dst, src, bytes, kind, stream);
+        };
+        SURR_HIP(cp(m->embed, tensors[0], V * d * e));
+        for (int l = 0; l < c.n_layers; ++l) {
+            const void* const* t = tensors + 1 + 9 * l;
+            char* qkv = static_cast<char*>(m->layers[l].w_qkv);
+            SURR_HIP(cp(m->layers[l].attn_norm, t[0], 4 * d));
+            SURR_HIP(cp(qkv, t[1], dq * d * e));
+            SURR_HIP(cp(qkv + dq * d * e, t[2], dkv * d * e));
+            SURR_HIP(cp(qkv + (dq + dkv) * d * e, t[3], dkv * d * e));
+            SURR_HIP(cp(m->layers[l].w_o, t[4], d * dq * e));
+            SURR_HIP(cp(m->layers[l].mlp_norm, t[5], 4 * d));
+            // gate/up interleave: block p of 32 gate rows goes to rows [64p, 64p+32), the
+            // matching up rows to [64p+32, 64p+64).
+            const size_t blk = 32 * d * e;
+            char* gu = static_cast<char*>(m->layers[l].w_gu);
+            SURR_HIP(hipMemcpy2DAsync(gu, 2 * blk, t[6], blk, blk, ff / 32, kind, stream));
+            SURR_HIP(hipMemcpy2DAsync(gu + blk, 2 * blk, t[7], blk, blk, ff / 32, kind, stream));
+            SURR_HIP(cp(m->layers[l].w_down, t[8], d * ff * e));
+        }
+        const int last = 1 + 9 * c.n_layers;
+        SURR_HIP(cp(m->final_norm, tensors[last], 4 * d));
+        SURR_HIP(cp(m->lm_head, tensors[last + 1], V * d * e));
+        // RoPE: theta = pos * base^(-2i/hd) in float64, stored as float32 (cos, sin).
+        for (int p = 0; p < c.max_pos; ++p)
+            for (size_t i = 0; i < half; ++i) {
+                const double th = (double)p * std::pow((double)c.rope_base, -2.0 * (double)i / c.head_dim);
+                cs[(size_t)p * half + i] = make_float2((float)std::cos(th), (float)std::sin(th));
+            }
+        SURR_HIP(hipMemcpyAsync(m->rope_cs, cs.data(), cs.size() * sizeof(float2),
+                                hipMemcpyHostToDevice, stream));
+        SURR_HIP(hipMemsetAsync(m->err_flag, 0, 4, stream));
+        SURR_HIP(hipStreamSynchronize(stream));
+        SURR_HIP(hipEventCreateWithFlags(&m->staged, hipEventDisableTiming));
+        return SURR_OK;
+    };
+    const surrogate_status st = body();
+    if (st != SURR_OK) {
+        hipStreamSynchronize(stream);
+        surrogate_free(m);
+        return st;
+    }
+    *out = m;
+    return SURR_OK;
+}
+
+surrogate_status surrogate_get_config(const surrogate_model* m, surrogate_config* out) {
+    if (!m || !out) return fail(SURR_E_INVALID_ARG, "null argument");
+    *out = m->cfg;
+    return SURR_OK;
+}
+
+surrogate_status surrogate_workspace_size(const surrogate_model* m, int32_t batch,
+                                          int64_t total_tokens, int32_t max_len, size_t* bytes) {
+    if (!m || !bytes) return fail(SURR_E_INVALID_ARG, "null argument");
+    if (batch < 1 || total_tokens < batch || max_len < 1 || max_len > m->cfg.max_pos ||
+        total_tokens > (int64_t)batch * max_len)
+        return fail(SURR_E_SHAPE, "need 1 <= batch <= total_tokens <= batch * max_len, max_len <= max_pos");
+    *bytes = layout(m, batch, total_tokens).total;
+    return SURR_OK;
+}
+
+surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens_d,
+                                       int64_t row_stride, const int32_t* lengths_h,
+                                       int32_t batch, const int32_t* verdict_ids_h,
+                                       int32_t n_verdict, void* workspace_d,
+                                       size_t workspace_bytes, float* logprobs_d, float* probs_d,
+                                       float* confidence_d, int32_t* verdict_d,
+                                       hipStream_t stream) {
+    if (!m || !tokens_d || !lengths_h || !verdict_ids_h || !workspace_d || !logprobs_d ||
+        !confidence_d)
+        return fail(SURR_E_INVALID_ARG, "null argument");
+    const surrogate_config& c = m->cfg;
+    if (batch < 1) return fail(SURR_E_INVALID_ARG, "batch must be >= 1");
+    if (n_verdict < 1 || n_verdict > 16) return fail(SURR_E_INVALID_ARG, "n_verdict must be in [1, 16]");
+    for (int i = 0; i < n_verdict; ++i) {
+        if (verdict_ids_h[i] < 0 || verdict_ids_h[i] >= c.vocab)
+            return fail(SURR_E_INVALID_ARG, "verdict id out of range");
+        for (int j = 0; j < i; ++j)
+            if (verdict_ids_h[j] == verdict_ids_h[i]) return fail(SURR_E_INVALID_ARG, "duplicate verdict id");
+    }
+    if (row_stride < 1) return fail(SURR_E_INVALID_ARG, "row_stride must be >= 1");
+    const int64_t cap = std::min<int64_t>(row_stride, c.max_pos);
+    int64_t T = 0;
+    for (int b = 0; b < batch; ++b) {
+        if (lengths_h[b] < 1 || lengths_h[b] > cap)
+            return fail(SURR_E_SHAPE, "length of prompt " + std::to_string(b) + " outside [1, min(row_stride, max_pos)]");
+        T += lengths_h[b];
+    }
+    if (T > INT32_MAX) return fail(SURR_E_SHAPE, "total tokens exceed 2^31 - 1");
+    if (reinterpret_cast<uintptr_t>(workspace_d) % kAlign) return fail(SURR_E_INVALID_ARG, "workspace must be 256-byte aligned");
+    const WsLayout w = layout(m, batch, T);
+    if (workspace_bytes < w.total)
+        return fail(SURR_E_WORKSPACE, "workspace needs " + std::to_string(w.total) + " bytes");
+
+    // ---- plan: prompt offsets, last rows, verdict ids, attention work lists
+    const int qt = surr::attention_q_tile(m->act);
+    std::vector<int32_t> cu(batch + 1, 0), last(batch);
+    for (int b = 0; b < batch; ++b) {
+        cu[b + 1] = cu[b] + lengths_h[b];
+        last[b] = cu[b + 1] - 1;
+    }
+    std::vector<int2> work, work_last(batch);
+    for (int b = 0; b < batch; ++b) {
+        for (int t = 0; t * qt < lengths_h[b]; ++t) work.push_back(make_int2(b, t));
+        work_last[b] = make_int2(b, (lengths_h[b] - 1) / qt);
+    }
+    // Longest key range first, so the big causal tiles start early; stable for
+    // a deterministic order.
+    auto kv_len = [&](const int2& it) { return std::min(lengths_h[it.x], (it.y + 1) * qt); };
+    std::stable_sort(work.begin(), work.end(),
+                     [&](const int2& a, const int2& b) { return kv_len(a) > kv_len(b); });
+
+    const size_t meta_bytes = w.pos;  // cu .. work_last are contiguous from offset 0
+    {
+        std::lock_guard<std::mutex> lock(m->mu);
+        if (m->staged_pending) SURR_HIP(hipEventSynchronize(m->staged));
+        m->staged_pending = false;
+        if (m->pinned_bytes < meta_bytes) {
+            if (m->pinned) SURR_HIP(hipHostFree(m->pinned));
+            m->pinned = nullptr;
+            m->pinned_bytes = 0;
+            if (hipHostMalloc(&m->pinned, meta_bytes, hipHostMallocDefault) != hipSuccess)
+                return fail(SURR_E_OOM, "pinned staging buffer");
+            m->pinned_bytes = meta_bytes;
+        }
+        char* P = static_cast<char*>(m->pinned);
+        std::memcpy(P + w.cu, cu.data(), 4 * cu.size());
+        std::memcpy(P + w.last, last.data(), 4 * last.size());
+        std::memcpy(P + w.vid, verdict_ids_h, 4 * (size_t)n_verdict);
+        std::memcpy(P + w.work, work.data(), 8 * work.size());
+        std::memcpy(P + w.work_last, work_last.data(), 8 * work_last.size());
+        SURR_HIP(hipMemcpyAsync(workspace_d, P, meta_bytes, hipMemcpyHostToDevice, stream));
+        SURR_HIP(hipEventRecord(m->staged, stream));
+        m->staged_pending = true;
+    }
+
+    char* W = static_cast<char*>(workspace_d);
+    const int32_t* d_cu = reinterpret_cast<const int32_t*>(W + w.cu);
+    const int32_t* d_last = reinterpret_cast<const int32_t*>(W + w.last);
+    const int32_t* d_vid = reinterpret_cast<const int32_t*>(W + w.vid);
+    const int2* d_work = reinterpret_cast<const int2*>(W + w.work);
+    const int2* d_work_last = reinterpret_cast<const int2*>(W + w.work_last);
+    int32_t* d_pos = reinterpret_cast<int32_t*>(W + w.pos);
+    float* x = reinterpret_cast<float*>(W + w.x);
+    void* h = W + w.h;
+    void* qkv = W + w.qkv;
+    void* o = W + w.o;
+    void* u = W + w.u;
+    float* gu = reinterpret_cast<float*>(W + w.gu);
+    void* o_last = W + w.o_last;
+    float* x_last = reinterpret_cast<float*>(W + w.x_last);
+    void* h_last = W + w.h_last;
+    void* u_last = W + w.u_last;
+    float* gu_last = reinterpret_cast<float*>(W + w.gu_last);
+    void* y = W + w.y;
+    float* logits = reinterpret_cast<float*>(W + w.logits);
+
+    const Act a = m->act;
+    const int d = c.d_model, ff = c.d_ff, nq = c.n_q_heads, nkv = c.n_kv_heads, hd = c.head_dim;
+    const int dq = (int)m->d_q(), dqkv = (int)m->d_qkv();
+    const int Ti = (int)T;
+
+    // Phase bracketing for the measurement hook (a no-op unless profiling is on).
+    auto mark = [&](int phase) -> hipError_t {
+        if (!m->profiling) return hipSuccess;
+        while (m->ev_used + 2 > m->ev_pool.size()) {
+            hipEvent_t e;
+            hipError_t r = hipEventCreate(&e);
+            if (r != hipSuccess) return r;
+            m->ev_pool.push_back(e);
+        }
+        m->rec.emplace_back(phase, m->ev_used);
+        const hipEvent_t e0 = m->ev_pool[m->ev_used];
+        m->ev_used += 2;
+        return hipEventRecord(e0, stream);
+    };
+    auto done = [&]() -> hipError_t {
+        if (!m->profiling) return hipSuccess;
+        return hipEventRecord(m->ev_pool[m->rec.back().second + 1], stream);
+    };
+#define SURR_PHASE_RUN(phase, expr)  \
+    do {                             \
+        SURR_HIP(mark(phase));       \
+        SURR_HIP(expr);              \
+        SURR_HIP(done());            \
+    } while (0)
+
+    auto mlp = [&](const LayerW& L, void* hin, void* uout, float* gtmp, float* xres, int M) -> surrogate_status {
+        if (a == Act::BF16) {
+            SURR_PHASE_RUN(SURR_PHASE_GEMM_GATE_UP, surr::launch_gemm(a, Epi::SwiGLU, hin, d, L.w_gu, d, uout, ff, M, 2 * ff, d, stream));
+        } else {
+            SURR_PHASE_RUN(SURR_PHASE_GEMM_GATE_UP, surr::launch_gemm(a, Epi::StoreF32, hin, d, L.w_gu, d, gtmp, 2 * ff, M, 2 * ff, d, stream));
+            SURR_PHASE_RUN(SURR_PHASE_GEMM_GATE_UP, surr::launch_swiglu_f32(gtmp, static_cast<float*>(uout), M, ff, stream));
+        }
+        SURR_PHASE_RUN(SURR_PHASE_GEMM_DOWN, surr::launch_gemm(a, Epi::ResidAddF32, uout, ff, L.w_down, ff, xres, d, M, d, ff, stream));
+        return SURR_OK;
+    };
+
+    SURR_PHASE_RUN(SURR_PHASE_EMBED, surr::launch_embed(a, tokens_d, row_stride, d_cu, batch, T, m->embed, d, c.vocab, x, d_pos, m->err_flag, stream));
+    for (int l = 0; l < c.n_layers; ++l) {
+        const LayerW& L = m->layers[l];
+        const bool final_layer = l == c.n_layers - 1;
+        SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x, d, nullptr, T, L.attn_norm, d, c.rms_eps, h, d, stream));
+        SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreAct, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream));
+        SURR_PHASE_RUN(SURR_PHASE_ROPE, surr::launch_rope(a, qkv, dqkv, T, d_pos, nq + nkv, hd, m->rope_cs, stream));
+        if (!final_layer) {
+            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, o, dq, d_cu, d_work, (int)work.size(), nq, nkv, hd, stream));
+            SURR_PHASE_RUN(SURR_PHASE_GEMM_O, surr::launch_gemm(a, Epi::ResidAddF32, o, dq, L.w_o, dq, x, d, Ti, d, dq, stream));
+            SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x, d, nullptr, T, L.mlp_norm, d, c.rms_eps, h, d, stream));
+            const surrogate_status st = mlp(L, h, u, gu, x, Ti);
+            if (st != SURR_OK) return st;
+        } else {
+            // Only the last position of each prompt feeds the LM head: K/V above cover
+            // every token; attention, O projection and MLP run for the last rows only.
+            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, o, dq, d_cu, d_work_last, batch, nq, nkv, hd, stream));
+            SURR_PHASE_RUN(SURR_PHASE_GATHER, surr::launch_gather_rows(o, dq, d_last, batch, dq, (int)m->esz, o_last, dq, stream));
+            SURR_PHASE_RUN(SURR_PHASE_GATHER, surr::launch_gather_rows(x, d, d_last, batch, d, 4, x_last, d, stream));
+            SURR_PHASE_RUN(SURR_PHASE_GEMM_O, surr::launch_gemm(a, Epi::ResidAddF32, o_last, dq, L.w_o, dq, x_last, d, batch, d, dq, stream));
+            SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, L.mlp_norm, d, c.rms_eps, h_last, d, stream));
+            const surrogate_status st = mlp(L, h_last, u_last, gu_last, x_last, batch);
+            if (st != SURR_OK) return st;
+        }
+    }
+    SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, m->final_norm, d, c.rms_eps, y, d, stream));
+    SURR_PHASE_RUN(SURR_PHASE_LM_HEAD, surr::launch_gemm(a, Epi::StoreF32, y, d, m->lm_head, d, logits, c.vocab, batch, c.vocab, d, stream));
+    SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_verdict(logits, c.vocab, batch, c.vocab, d_vid, n_verdict, logprobs_d, probs_d, confidence_d, verdict_d, stream));
+#undef SURR_PHASE_RUN
+    return SURR_OK;
+}
+
+surrogate_status surrogate_select(const float* confidence_d, int32_t n, surrogate_select_mode mode,
+                                  float threshold, int32_t budget_k, int32_t* defer_idx_d,
+                                  int32_t* accept_idx_d, int32_t* counts_d, hipStream_t stream) {
+    if (!confidence_d || !defer_idx_d || !accept_idx_d || !counts_d)
+        return fail(SURR_E_INVALID_ARG, "null argument");
+    if (n < 1 || n > 65536) return fail(SURR_E_INVALID_ARG, "n must be in [1, 65536]");
+    if (mode != SURR_SELECT_THRESHOLD && mode != SURR_SELECT_BUDGET)
+        return fail(SURR_E_INVALID_ARG, "unknown select mode");
+    if (mode == SURR_SELECT_BUDGET && budget_k < 0) return fail(SURR_E_INVALID_ARG, "budget_k must be >= 0");
+    const int k = mode == SURR_SELECT_BUDGET ? std::min(budget_k, n) : 0;
+    SURR_HIP(surr::launch_select(confidence_d, n, mode == SURR_SELECT_BUDGET ? 1 : 0, threshold, k,
+                                 defer_idx_d, defer_idx_d, accept_idx_d, counts_d, stream));
+    return SURR_OK;
+}
+
+surrogate_status surrogate_device_status(surrogate_model* m, hipStream_t stream) {
+    if (!m) return fail(SURR_E_INVALID_ARG, "null argument");
+    int32_t flag = 0;
+    SURR_HIP(hipStreamSynchronize(stream));
+    SURR_HIP(hipMemcpy(&flag, m->err_flag, 4, hipMemcpyDeviceToHost));
+    if (flag) {
+        SURR_HIP(hipMemset(m->err_flag, 0, 4));
+        return fail(SURR_E_TOKEN_RANGE, "a token id outside [0, vocab) was read as id 0");
+    }
+    return SURR_OK;
+}
+
+surrogate_status surrogate_profile_enable(surrogate_model* m, int32_t enable) {
+    if (!m) return fail(SURR_E_INVALID_ARG, "null argument");
+    m->profiling = enable != 0;
+    return SURR_OK;
+}
+
+surrogate_status surrogate_profile_collect(surrogate_model* m, double* ms_out, int64_t* launches_out) {
+    if (!m || !ms_out || !launches_out) return fail(SURR_E_INVALID_ARG, "null argument");
+    for (int p = 0; p < SURR_N_PHASES; ++p) {
+        ms_out[p] = 0.0;
+        launches_out[p] = 0;
+    }
+    for (const auto& r : m->rec) {
+        float ms = 0.f;
+        SURR_HIP(hipEventSynchronize(m->ev_pool[r.second + 1]));
+        SURR_HIP(hipEventElapsedTime(&ms, m->ev_pool[r.second], m->ev_pool[r.second + 1]));
+        ms_out[r.first] += ms;
+        launches_out[r.first] += 1;
+    }
+    m->rec.clear();
+    m->ev_used = 0;
+    return SURR_OK;
+}
+
+const char* surrogate_status_string(surrogate_status s) {
+    switch (s) {
+        case SURR_OK: return "ok";
+        case SURR_E_INVALID_ARG: return "invalid argument";
+        case SURR_E_SHAPE: return "unsupported shape or length";
+        case SURR_E_TOKEN_RANGE: return "token id out of range";
+        case SURR_E_OOM: return "out of memory";
+        case SURR_E_HIP: return "HIP runtime error";
+        case SURR_E_WEIGHTS: return "weights do not match the config";
+        case SURR_E_WORKSPACE: return "workspace too small";
+    }
+    return "unknown status";
+}
+
+const char* surrogate_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared entry point,
+and rejects bad arguments synchronously (before any device work)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2605_31464_amd import binding as B
+from paper_2605_31464_amd import synth
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "surrogate.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(surrogate_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.lib()
+    names = declared_functions()
+    assert len(names) == 13
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(B.EXPORTS)
+
+
+def test_tensor_layout_matches_the_synthetic_generator():
+    for w in synth.CONFIGS.values():
+        cfg = B.make_config(w.shape)
+        specs = synth.tensor_specs(w.shape)
+        assert B.surrogate_tensor_count(cfg) == len(specs)
+        for i, (name, rows, cols, is_norm) in enumerate(specs):
+            r, c, dt = B.surrogate_tensor_shape(cfg, i)
+            assert (r, c) == (rows, cols), name
+            assert dt == (B.SURR_F32 if is_norm or w.shape.dtype == "f32" else B.SURR_BF16)
+
+
+@pytest.mark.parametrize("bad", [dict(n_q_heads=5, n_kv_heads=2), dict(head_dim=48),
+                                 dict(vocab=1000), dict(d_ff=100), dict(max_pos=0),
+                                 dict(n_layers=0)])
+def test_unsupported_configs_are_rejected(bad):
+    shape = synth.CONFIGS["small"].shape.replace(**bad)
+    cfg = B.make_config(shape)
+    with pytest.raises(B.SurrogateError) as e:
+        B.surrogate_tensor_shape(cfg, 0)
+    assert e.value.status in (B.SURR_E_SHAPE,)
+
+
+def test_load_weights_rejects_wrong_tensor_count_before_allocating():
+    cfg = B.make_config(synth.CONFIGS["tiny"].shape)
+    ptrs = (ctypes.c_void_p * 3)(1, 1, 1)
+    h = ctypes.c_void_p()
+    st = B.lib().surrogate_load_weights(ctypes.byref(cfg), ptrs, 3, 0, None, ctypes.byref(h))
+    assert st == B.SURR_E_WEIGHTS and not h.value
+    assert b"expected" in B.lib().surrogate_last_error()
+
+
+def test_select_rejects_bad_arguments_synchronously():
+    L = B.lib()
+    p = ctypes.c_void_p(16)
+    assert L.surrogate_select(p, 0, 0, 0.5, 0, p, p, p, None) == B.SURR_E_INVALID_ARG
+    assert L.surrogate_select(p, 65537, 0, 0.5, 0, p, p, p, None) == B.SURR_E_INVALID_ARG
+    assert L.surrogate_select(p, 4, 7, 0.5, 0, p, p, p, None) == B.SURR_E_INVALID_ARG
+    assert L.surrogate_select(p, 4, 1, 0.5, -1, p, p, p, None) == B.SURR_E_INVALID_ARG
+    assert L.surrogate_select(None, 4, 0, 0.5, 0, p, p, p, None) == B.SURR_E_INVALID_ARG
+
+
+def test_score_pairs_rejects_null_model():
+    L = B.lib()
+    p = ctypes.c_void_p(256)
+    lens = np.array([3], np.int32)
+    vid = np.array([1], np.int32)
+    st = L.surrogate_score_pairs(None, p, 4, lens.ctypes.data, 1, vid.ctypes.data, 1, p, 1 << 20,
+                                 p, None, p, None, None)
+    assert st == B.SURR_E_INVALID_ARG
+
+
+def test_status_strings():
+    L = B.lib()
+    for s in range(0, -8, -1):
+        assert L.surrogate_status_string(s)
+    assert L.surrogate_status_string(-3) == b"token id out of range"

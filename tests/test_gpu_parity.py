@@ -1,0 +1,217 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Tolerances: verdict log-probs (full-vocabulary log-softmax) and the renormalised
+verdict probabilities within 1e-4 absolute for the float32 model and 3e-2 for bf16
+models; identical predicted verdicts wherever the oracle's top-1/top-2 log-prob margin
+exceeds 0.1 nats; bit-exact deferral sets on a given confidence vector.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import select as osel
+from oracle import transformer as ot
+from paper_2605_31464_amd import binding as B
+from paper_2605_31464_amd import synth
+
+from conftest import arch_of
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+TOL = {"f32": 1e-4, "bf16": 3e-2}
+
+
+def make_scorer(shape, gain_std=0.0, seed=0):
+    W = synth.make_weights(shape, seed=seed, gain_std=gain_std)
+    names = [s[0] for s in synth.tensor_specs(shape)]
+    return B.Scorer(shape, W, names, DEV), W
+
+
+def padded(prompts, pad=0):
+    L = np.array([len(p) for p in prompts], np.int32)
+    tok = np.full((len(prompts), int(L.max())), pad, np.int32)
+    for i, p in enumerate(prompts):
+        tok[i, : len(p)] = p
+    return tok, L
+
+
+def oracle_for(shape, W, tok, L, vid, rows=None):
+    rows = range(len(L)) if rows is None else rows
+    return ot.score(arch_of(shape), W, [tok[i, : L[i]] for i in rows], vid)
+
+
+def assert_parity(out, ref, tol, rows=None):
+    rows = slice(None) if rows is None else list(rows)
+    lp = out["logprobs"].cpu().numpy()[rows]
+    p = out["p"].cpu().numpy()[rows]
+    q = out["confidence"].cpu().numpy()[rows]
+    v = out["verdict"].cpu().numpy()[rows]
+    err = np.abs(lp - ref["logprobs"]).max()
+    print(f"max |lp - oracle| = {err:.3e} (tol {tol})", flush=True)
+    assert err <= tol
+    assert np.abs(p - ref["p"]).max() <= tol
+    assert np.abs(q - ref["confidence"]).max() <= tol
+    sure = ref["margin"] > 0.1
+    assert np.array_equal(v[sure], ref["verdict"][sure])
+    # the read-out itself is exact given the kernel's own log-probs
+    np.testing.assert_allclose(p.sum(axis=1), 1.0, atol=1e-5)
+    assert np.array_equal(q, p.max(axis=1))
+
+
+def rng_prompts(vocab, lengths, seed):
+    rng = np.random.default_rng(seed)
+    cdf = synth.zipf_cdf(vocab)
+    return [np.minimum(np.searchsorted(cdf, rng.random(n), side="right"), vocab - 1).astype(np.int32)
+            for n in lengths]
+
+
+# ---------------------------------------------------------------- selection
+def select_cases():
+    rng = np.random.default_rng(5)
+    for n in (1, 2, 7, 128, 1000, 4097, 65536):
+        q = rng.random(n).astype(np.float32)
+        if n > 2:
+            q[rng.integers(0, n, max(1, n // 10))] = np.nan
+            q[rng.integers(0, n, max(1, n // 5))] = np.float32(0.5)
+            q[rng.integers(0, n, max(1, n // 20))] = -0.0
+            q[rng.integers(0, n, max(1, n // 20))] = 0.0
+        yield n, q
+
+
+@pytest.mark.parametrize("n,q", list(select_cases()), ids=lambda x: str(x) if np.isscalar(x) else "")
+def test_select_matches_oracle_bit_exact(n, q):
+    dq = torch.from_numpy(q).to(DEV)
+    for tau in (0.0, 0.5, 0.7, 1.0, 1.5):
+        d, a, c = B.surrogate_select(dq, B.SURR_SELECT_THRESHOLD, threshold=tau)
+        rd, ra = osel.select_threshold(q, tau)
+        c = c.cpu().numpy()
+        assert list(c) == [len(rd), len(ra)]
+        assert np.array_equal(d.cpu().numpy()[: c[0]], rd)
+        assert np.array_equal(a.cpu().numpy()[: c[1]], ra)
+    for k in sorted({0, 1, n // 5, n - 1, n, n + 7}):
+        if k < 0:
+            continue
+        d, a, c = B.surrogate_select(dq, B.SURR_SELECT_BUDGET, budget_k=k)
+        rd, ra = osel.select_budget(q, k)
+        c = c.cpu().numpy()
+        assert list(c) == [len(rd), len(ra)]
+        assert np.array_equal(d.cpu().numpy()[: c[0]], rd)
+        assert np.array_equal(a.cpu().numpy()[: c[1]], ra)
+
+
+# ---------------------------------------------------------------- tiny fp32 model
+@pytest.fixture(scope="module")
+def tiny():
+    return make_scorer(synth.CONFIGS["tiny"].shape, gain_std=0.1)
+
+
+def test_tiny_config_matches_oracle(tiny):
+    scorer, W = tiny
+    w = synth.CONFIGS["tiny"]
+    tok, L = synth.make_prompts(w)
+    vid = synth.verdict_ids(w)
+    out = scorer.score(tok, L, vid)
+    assert_parity(out, oracle_for(w.shape, W, tok, L, vid), TOL["f32"])
+    d, a, c = B.surrogate_select(out["confidence"], B.SURR_SELECT_THRESHOLD, threshold=w.select[1])
+    rd, ra = osel.select_threshold(out["confidence"].cpu().numpy(), w.select[1])
+    assert np.array_equal(d.cpu().numpy()[: c[0]], rd)
+
+
+def test_tiny_ragged_edges_match_oracle(tiny):
+    scorer, W = tiny
+    shape = synth.CONFIGS["tiny"].shape
+    lengths = [1, 2, 63, 64, 65, 127, 128, 129, 300, shape.max_pos]
+    tok, L = padded(rng_prompts(shape.vocab, lengths, 7), pad=shape.vocab + 3)
+    for vid in ([5], [0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 511]):
+        out = scorer.score(tok, L, vid)
+        assert_parity(out, oracle_for(shape, W, tok, L, vid), TOL["f32"])
+    assert B.surrogate_device_status(scorer.model) == B.SURR_OK  # padding never read
+
+
+def test_out_of_range_token_raises_sticky_error(tiny):
+    scorer, W = tiny
+    tok, L = padded([np.array([1, 2, 600, 3], np.int32)])
+    scorer.score(tok, L, [0, 1])
+    assert B.surrogate_device_status(scorer.model) == B.SURR_E_TOKEN_RANGE
+    assert B.surrogate_device_status(scorer.model) == B.SURR_OK  # cleared
+
+
+def test_bad_lengths_and_workspace_are_rejected(tiny):
+    scorer, W = tiny
+    tok = torch.zeros((2, 8), dtype=torch.int32, device=DEV)
+    out = torch.empty(2, 1, device=DEV)
+    conf = torch.empty(2, device=DEV)
+    ws = scorer.ensure_workspace(2, 16, 8)
+    for L in ([0, 3], [9, 3]):
+        with pytest.raises(B.SurrogateError) as e:
+            B.surrogate_score_pairs(scorer.model, tok, L, [1], ws, out, conf)
+        assert e.value.status == B.SURR_E_SHAPE
+    with pytest.raises(B.SurrogateError) as e:
+        B.surrogate_score_pairs(scorer.model, tok, [8, 8], [1], ws[:100], out, conf)
+    assert e.value.status == B.SURR_E_WORKSPACE
+    with pytest.raises(B.SurrogateError) as e:
+        B.surrogate_score_pairs(scorer.model, tok, [8, 8], [1, 1], ws, out, conf)
+    assert e.value.status == B.SURR_E_INVALID_ARG
+
+
+# ---------------------------------------------------------------- bf16 models
+@pytest.fixture(scope="module")
+def small3():
+    shape = synth.CONFIGS["small"].shape.replace(n_layers=3)
+    return (shape,) + make_scorer(shape, gain_std=0.1)
+
+
+def test_small_shape_bf16_ragged_matches_oracle(small3):
+    shape, scorer, W = small3
+    lengths = [1, 5, 127, 128, 129, 255, 256, 513, 700]
+    tok, L = padded(rng_prompts(shape.vocab, lengths, 11))
+    vid = [shape.vocab - 2, shape.vocab - 1]
+    out = scorer.score(tok, L, vid)
+    assert_parity(out, oracle_for(shape, W, tok, L, vid), TOL["bf16"])
+
+
+def test_bf16_batch_invariance_and_determinism(small3):
+    shape, scorer, W = small3
+    lengths = [300, 17, 129, 64]
+    prompts = rng_prompts(shape.vocab, lengths, 12)
+    tok, L = padded(prompts, pad=-5)
+    vid = [3, 4, 5]
+    a = scorer.score(tok, L, vid)
+    b = scorer.score(tok, L, vid)
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+    for i in range(len(L)):
+        t1, l1 = padded([prompts[i]])
+        s = scorer.score(t1, l1, vid)
+        assert torch.equal(s["logprobs"][0], a["logprobs"][i])
+    perm = [2, 0, 3, 1]
+    tp, lp_ = padded([prompts[i] for i in perm])
+    c = scorer.score(tp, lp_, vid)
+    assert torch.equal(c["logprobs"], a["logprobs"][perm])
+    assert B.surrogate_device_status(scorer.model) == B.SURR_OK
+
+
+def test_hd128_gqa_shape_matches_oracle():
+    shape = synth.CONFIGS["1p5b"].shape.replace(n_layers=2)
+    scorer, W = make_scorer(shape, gain_std=0.1)
+    lengths = [1, 130, 257, 600]
+    tok, L = padded(rng_prompts(shape.vocab, lengths, 13))
+    vid = list(range(shape.vocab - 5, shape.vocab))
+    out = scorer.score(tok, L, vid)
+    assert_parity(out, oracle_for(shape, W, tok, L, vid), TOL["bf16"])
+
+
+def test_small_config_full_depth_sampled_prompts():
+    w = synth.CONFIGS["small"]
+    scorer, W = make_scorer(w.shape)
+    tok, L = synth.make_prompts(w)
+    vid = synth.verdict_ids(w)
+    out = scorer.score(tok, L, vid)
+    rows = [int(np.argmin(L)), 0]
+    assert_parity(out, oracle_for(w.shape, W, tok, L, vid, rows), TOL["bf16"], rows)
+    k = w.budget_k
+    d, a, c = B.surrogate_select(out["confidence"], B.SURR_SELECT_BUDGET, budget_k=k)
+    rd, ra = osel.select_budget(out["confidence"].cpu().numpy(), k)
+    assert np.array_equal(d.cpu().numpy()[: c[0]], rd) and len(rd) == k
