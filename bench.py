@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Throughput of batched forecast scoring on one MI355X.
+
+One step = one prefill-only scoring pass over a batch of ragged kernel-pair prompts
+(surrogate_score_pairs: embedding, all decoder layers, last-position LM head with the
+full-vocabulary log-softmax, verdict read-out) followed by the deferral step
+(surrogate_select).  Inputs are seeded synthetic prompts and random weights of the
+named shape, resident in HBM before the timed region starts.
+
+Default workload: the 7B-shape bf16 decoder (28 layers, d_model 3584, 28/4 heads of
+128, d_ff 18944, vocab 131072), 128 prompts with lognormal lengths (median 3072,
+sigma 0.5, clipped to [1024, 8192]), 2 verdict tokens, budget deferral of
+floor(0.2 * 128) = 25 candidates.
+
+Prints one JSON line.  `value` is forecast pairs/s; prefill tokens/s and the fraction
+of the bf16 MFMA peak are reported beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16 = 2.5e15  # MI355X dense bf16 MFMA, FLOP/s
+PEAK_HBM = 8.0e12   # MI355X HBM3E, B/s
+METRIC = "forecast pairs/sec + prefill tokens/sec at 7B shape; % bf16 MFMA peak"
+
+
+def flops_per_prompt(s, L: np.ndarray) -> np.ndarray:
+    """Algorithmic FLOPs of scoring one prompt of length L: causal triangle only, final
+    layer pruned to the K/V projection plus the last row, LM head at the last row."""
+    d, dq, dkv, ff = s.d_model, s.d_q, s.d_kv, s.d_ff
+    L = L.astype(np.float64)
+    c_lin = 2 * d * (dq + 2 * dkv) + 2 * dq * d + 6 * d * ff
+    c_att = 2 * s.n_q_heads * s.head_dim * L * (L + 1)
+    return ((s.n_layers - 1) * (c_lin * L + c_att) + 4 * d * dkv * L + (c_lin - 4 * d * dkv)
+            + 4 * s.n_q_heads * s.head_dim * L + 2 * d * s.vocab)
+
+
+def cpu_baseline(shape, W, tok, L, vid) -> dict:
+    """Time the float64 oracle on a bounded sample of the same workload and scale it to
+    pairs/s: layers 0-1 of the model over the first 256 tokens of the shortest prompt,
+    plus one last-position head; scaled linearly in layers and tokens to the batch's
+    mean prompt length."""
+    from oracle import transformer as ot
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()
+                       if i.get("user_api") == "blas"] or [os.cpu_count() or 1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    n_sample_layers, n_tok = 2, 256
+    i0 = int(np.argmin(L))
+    prompt = tok[i0, : min(n_tok, int(L[i0]))]
+    arch = dict(n_layers=n_sample_layers, d_model=shape.d_model, n_q_heads=shape.n_q_heads,
+                n_kv_heads=shape.n_kv_heads, head_dim=shape.head_dim, d_ff=shape.d_ff,
+                vocab=shape.vocab, rope_base=shape.rope_base, rms_eps=shape.rms_eps)
+    t0 = time.perf_counter()
+    xs = ot.forward_hidden(arch, W, [prompt])
+    t1 = time.perf_counter()
+    z = ot.last_position_logits(arch, W, xs)
+    ot.log_softmax_full(z[0])
+    t2 = time.perf_counter()
+    per_pair = (t1 - t0) * (shape.n_layers / n_sample_layers) * (float(L.mean()) / len(prompt)) \
+        + (t2 - t1)
+    return {"value": 1.0 / per_pair, "unit": "pairs/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"float64 oracle, layers 0-{n_sample_layers - 1} of {shape.n_layers} over "
+                      f"the first {len(prompt)} tokens of prompt {i0} plus one LM head "
+                      f"({t2 - t0:.1f} s measured), scaled linearly to {shape.n_layers} layers "
+                      f"and the mean length {float(L.mean()):.0f}",
+            "tokens_per_s": float(L.mean()) / per_pair,
+            "cpu": platform.processor() or platform.machine()}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="7b", help="tiny | small | 1p5b | 7b | 14b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true",
+                    help="skip the per-phase HIP-event timing (the roofline block)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build scores on exactly one GPU; runs with --gpus above 1 are "
+              "not supported (prompts shard by data parallelism, which is not built here).",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2605_31464_amd import binding as B
+    from paper_2605_31464_amd import synth
+
+    w = synth.CONFIGS[args.config]
+    s = w.shape
+    t_setup = time.perf_counter()
+    W = synth.make_weights(s)
+    names = [x[0] for x in synth.tensor_specs(s)]
+    tok_np, L = synth.make_prompts(w)
+    vid = synth.verdict_ids(w)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = B.make_config(s)
+    model = B.surrogate_load_weights(cfg, [W[n] for n in names])
+    B_ = len(L)
+    T = int(L.sum())
+    tok = torch.from_numpy(tok_np).to(dev)
+    ws = torch.empty(B.surrogate_workspace_size(model, B_, T, int(L.max())), dtype=torch.uint8,
+                     device=dev)
+    nv = len(vid)
+    lp = torch.empty(B_, nv, device=dev)
+    p = torch.empty(B_, nv, device=dev)
+    conf = torch.empty(B_, device=dev)
+    verdict = torch.empty(B_, dtype=torch.int32, device=dev)
+    d_idx = torch.empty(B_, dtype=torch.int32, device=dev)
+    a_idx = torch.empty(B_, dtype=torch.int32, device=dev)
+    counts = torch.empty(2, dtype=torch.int32, device=dev)
+    if w.select[0] == "budget":
+        mode, tau, k = B.SURR_SELECT_BUDGET, 0.0, w.budget_k
+    else:
+        mode, tau, k = B.SURR_SELECT_THRESHOLD, w.select[1], 0
+    stream = torch.cuda.current_stream()
+    print(f"[bench] {w.name}: B={B_} T={T} setup {time.perf_counter() - t_setup:.1f}s",
+          file=sys.stderr, flush=True)
+
+    def step():
+        B.surrogate_score_pairs(model, tok, L, vid, ws, lp, conf, p, verdict, stream=stream)
+        B.surrogate_select(conf, mode, tau, k, d_idx, a_idx, counts, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if B.surrogate_device_status(model) != B.SURR_OK:
+        raise RuntimeError("device error during warm-up")
+    if not args.no_profile:
+        B.surrogate_profile_enable(model, True)
+        B.surrogate_profile_collect(model)  # start from zero
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step()
+        print(f"[bench] step {i + 1}/{args.steps} enqueued", file=sys.stderr, flush=True)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_s = ev0.elapsed_time(ev1) / 1e3
+    phases = B.surrogate_profile_collect(model) if not args.no_profile else {}
+    B.surrogate_profile_enable(model, False)
+
+    t_step = gpu_s / args.steps
+    flop = float(flops_per_prompt(s, L).sum())
+    out = {
+        "metric": METRIC,
+        "value": B_ / t_step,
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": t_step * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if s.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded Zipf(1.1) prompts, N(0,0.02) weights)",
+        "config": {"workload": w.name, "batch": B_, "total_tokens": T,
+                   "lengths": list(w.lengths), "n_verdict": nv,
+                   "select": f"{w.select[0]} {k if w.select[0] == 'budget' else tau}"},
+        "prefill_tokens_per_s": T / t_step,
+        "mfma_frac_of_peak": flop / t_step / PEAK_BF16,
+        "algorithmic_tflop_per_step": flop / 1e12,
+        "wall_s_timed": wall,
+    }
+    if phases:
+        out["phases_ms_per_step"] = {ph: ms / args.steps for ph, (ms, n) in phases.items() if n}
+        # Dominant kernel: the gate/up projection with its SwiGLU epilogue, one launch per
+        # non-final layer over all T tokens: 2 * T * (2 d_ff) * d_model FLOP per launch.
+        ms, n = phases["gemm_gate_up"]
+        if n:
+            per_launch = 2.0 * T * (2 * s.d_ff) * s.d_model
+            avg_s = ms / n / 1e3
+            ach = per_launch / avg_s
+            out["roofline"] = {"kernel": "gemm_bf16 SwiGLU epilogue (gate/up projection)",
+                               "bound": "mfma", "achieved": ach / 1e12,
+                               "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
+                               "frac": ach / PEAK_BF16, "traffic": None,
+                               "avg_launch_ms": avg_s * 1e3, "launches": n}
+    if not args.no_cpu_baseline:
+        print("[bench] timing the float64 oracle on a bounded sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(s, W, tok_np, L, vid)
+    print(json.dumps(out), flush=True)
+    B.surrogate_free(model)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -144,14 +144,14 @@ surrogate_status surrogate_device_status(surrogate_model *m, hipStream_t stream)
 /* Measurement hook.  Kernel phases of surrogate_score_pairs: */
 typedef enum {
     SURR_PHASE_EMBED = 0,     /* varlen token packing + embedding gather          */
-    SURR_PHASE_RMSNORM,       /* every RMSNorm (attention, MLP, final)             */
+    SURR_PHASE_RMSNORM,       /* RMSNorm over all tokens (attention, MLP)          */
     SURR_PHASE_GEMM_QKV,      /* fused QKV projection                              */
     SURR_PHASE_ROPE,          /* rotary embedding of q and k                       */
     SURR_PHASE_ATTENTION,     /* causal GQA prefill attention                      */
-    SURR_PHASE_GEMM_O,        /* output projection + residual                      */
-    SURR_PHASE_GEMM_GATE_UP,  /* gate/up projection + SwiGLU                       */
-    SURR_PHASE_GEMM_DOWN,     /* down projection + residual                        */
-    SURR_PHASE_GATHER,        /* last-position row gathers                         */
+    SURR_PHASE_GEMM_O,        /* output projection + residual, all tokens          */
+    SURR_PHASE_GEMM_GATE_UP,  /* gate/up projection + SwiGLU, all tokens           */
+    SURR_PHASE_GEMM_DOWN,     /* down projection + residual, all tokens            */
+    SURR_PHASE_LAST_ROWS,     /* final layer's row-pruned work + final RMSNorm     */
     SURR_PHASE_LM_HEAD,       /* last-position LM head GEMM                        */
     SURR_PHASE_LSE_VERDICT,   /* full-vocab log-softmax + verdict read-out         */
     SURR_N_PHASES

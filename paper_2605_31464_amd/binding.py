@@ -30,7 +30,7 @@ EXPORTS = ("surrogate_tensor_count", "surrogate_tensor_shape", "surrogate_load_w
            "surrogate_status_string", "surrogate_last_error", "surrogate_profile_enable",
            "surrogate_profile_collect")
 PHASES = ("embed", "rmsnorm", "gemm_qkv", "rope", "attention", "gemm_o", "gemm_gate_up",
-          "gemm_down", "gather", "lm_head", "lse_verdict")
+          "gemm_down", "last_rows", "lm_head", "lse_verdict")
 
 
 class SurrogateError(RuntimeError):

@@ -1,11 +1,11 @@
 // Projection GEMMs C = A[M,K] * B[N,K]^T with fused epilogues.
 //
 // bf16 path: v_mfma_f32_32x32x16_bf16 on a BM x BN workgroup tile (4 wavefronts, each
-// WM x WN), K in steps of 64.  Both operands are K-contiguous, so one 16-byte chunk of
-// a row is exactly the 8 consecutive k values an MFMA lane supplies.  Tiles go
-// global -> registers -> LDS (double buffered, one barrier per K step); LDS rows hold
-// 8 chunks whose order is XOR-swizzled by the row to spread the 16-byte reads over the
-// banks.  The MFMA is issued with the weight fragment as its A operand and the
+// WM x WN), K in steps of BK.  Both operands are K-contiguous, so one 16-byte chunk of
+// a row is exactly the 8 consecutive k values an MFMA lane supplies.  Tiles move from
+// HBM straight into LDS with global_load_lds_dwordx4 (no staging registers) through an
+// NST-stage ring, one barrier per K step; LDS rows hold BK/8 chunks whose order is
+// XOR-swizzled by the row to spread the 16-byte reads over the banks.  The MFMA is issued with the weight fragment as its A operand and the
 // activation fragment as its B operand, so each lane ends up owning one output row m
 // and runs of 4 consecutive output columns n - the shape the epilogues want (8- or
 // 16-byte stores, gate/up pairs and residual rows in one lane).
@@ -15,32 +15,49 @@
 #include "kernels.h"
 
 namespace surr {
-namespace {
+namespace gemm {
 
-constexpr int kBK = 64;
-
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int BK, int WM, int WN, int NST>
 struct Tile {
     static constexpr int WAVES_N = BN / WN;
     static_assert((BM / WM) * (BN / WN) == 4, "four wavefronts per workgroup");
     static constexpr int FM = WM / 32, FN = WN / 32;
-    static constexpr int A_LD = BM * 8 / 256;  // 16-byte chunks per thread per K step
-    static constexpr int B_LD = BN * 8 / 256;
-    static constexpr int STAGE = (BM + BN) * 8;  // uint4 slots per LDS stage
+    static constexpr int CH = BK / 8;               // 16-byte chunks per tile row
+    static constexpr int A_SLOTS = BM * CH, B_SLOTS = BN * CH;
+    static constexpr int STAGE = A_SLOTS + B_SLOTS;  // 16-byte LDS slots per stage
+    static constexpr int LOADS = STAGE / 256;        // DMA loads per thread per stage
+    static_assert(A_SLOTS % 64 == 0 && STAGE % 256 == 0, "whole wavefront loads");
+    static_assert(NST >= 2 && (NST - 2) * LOADS <= 63, "vmcnt range");
 };
 
-__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+// Chunk order inside an LDS row: XOR with row bits so 16 consecutive rows read at one
+// logical chunk land on 16 distinct 16-byte bank groups.
+template <int CH>
+__device__ __forceinline__ int swz(int row) {
+    if constexpr (CH == 8) return (row >> 1) & 7;
+    else return (row >> 2) & 3;
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N <= 63, "vmcnt");
+    // s_waitcnt simm16 on gfx9: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
 __device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); }
 
-template <int BM, int BN, int WM, int WN, Epi EPI>
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+
+template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restrict__ A,
                                                         int64_t lda,
                                                         const uint16_t* __restrict__ B,
                                                         int64_t ldb, void* __restrict__ C,
                                                         int64_t ldc, int M, int N, int K) {
-    using S = Tile<BM, BN, WM, WN>;
-    __shared__ uint4 lds[2 * S::STAGE];
+    using S = Tile<BM, BN, BK, WM, WN, NST>;
+    __shared__ uint4 lds[NST * S::STAGE];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / S::WAVES_N, wn = wave % S::WAVES_N;
 
@@ -56,25 +73,38 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restri
     const int tn = (pid % width) / gsz;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    // Thread tid moves chunk (tid & 7) of rows (tid >> 3) + 32 i.  Rows past M or N are
-    // clamped to the last valid row (their results are never stored).
-    const int c = tid & 7;
-    const uint16_t* a_src[S::A_LD];
-    const uint16_t* b_src[S::B_LD];
-    int a_dst[S::A_LD], b_dst[S::B_LD];
+    // Direct-to-LDS loads: wavefront `wave`, load j fills the 64 consecutive slots
+    // (wave * LOADS + j) * 64 + lane of a stage (the hardware places lane l's 16 bytes at
+    // slot base + l).  Slot -> (row, physical chunk) -> logical chunk via the swizzle;
+    // rows past M or N are clamped (their results are never stored).
+    const uint16_t* gsrc[S::LOADS];
 #pragma unroll
-    for (int i = 0; i < S::A_LD; ++i) {
-        const int r = (tid >> 3) + 32 * i;
-        a_src[i] = A + (int64_t)min(m0 + r, M - 1) * lda + c * 8;
-        a_dst[i] = r * 8 + (c ^ swz(r));
+    for (int j = 0; j < S::LOADS; ++j) {
+        const int slot = (wave * S::LOADS + j) * 64 + lane;
+        if (slot < S::A_SLOTS) {
+            const int r = slot / S::CH, c = (slot % S::CH) ^ swz<S::CH>(r);
+            gsrc[j] = A + (int64_t)min(m0 + r, M - 1) * lda + c * 8;
+        } else {
+            const int sb = slot - S::A_SLOTS;
+            const int r = sb / S::CH, c = (sb % S::CH) ^ swz<S::CH>(r);
+            gsrc[j] = B + (int64_t)min(n0 + r, N - 1) * ldb + c * 8;
+        }
     }
-#pragma unroll
-    for (int i = 0; i < S::B_LD; ++i) {
-        const int r = (tid >> 3) + 32 * i;
-        b_src[i] = B + (int64_t)min(n0 + r, N - 1) * ldb + c * 8;
-        b_dst[i] = (BM + r) * 8 + (c ^ swz(r));
-    }
-    uint4 ra[S::A_LD], rb[S::B_LD];
+
+    // One stage of direct-to-LDS loads (load j of wavefront `wave` fills the 64 slots
+    // starting at (wave * LOADS + j) * 64).  The builtin exists only in the device pass;
+    // the host pass compiles an empty body (it never runs kernel code).
+#if defined(__HIP_DEVICE_COMPILE__)
+#define SURR_ISSUE_STAGE(stage, k0)                                                          \
+    do {                                                                                     \
+        _Pragma("unroll") for (int j = 0; j < S::LOADS; ++j)                                 \
+            __builtin_amdgcn_global_load_lds(                                                \
+                gsrc[j] + (k0),                                                              \
+                (lds_ptr_t)(lds + (stage) * S::STAGE + (wave * S::LOADS + j) * 64), 16, 0, 0); \
+    } while (0)
+#else
+#define SURR_ISSUE_STAGE(stage, k0) ((void)(stage), (void)(k0))
+#endif
 
     f32x16 acc[S::FM][S::FN];
 #pragma unroll
@@ -82,41 +112,31 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restri
 #pragma unroll
         for (int j = 0; j < S::FN; ++j) acc[i][j] = f32x16{};
 
-    const int nk = K / kBK;
+    const int nk = K / BK;
 #pragma unroll
-    for (int i = 0; i < S::A_LD; ++i) ra[i] = *reinterpret_cast<const uint4*>(a_src[i]);
-#pragma unroll
-    for (int i = 0; i < S::B_LD; ++i) rb[i] = *reinterpret_cast<const uint4*>(b_src[i]);
-#pragma unroll
-    for (int i = 0; i < S::A_LD; ++i) lds[a_dst[i]] = ra[i];
-#pragma unroll
-    for (int i = 0; i < S::B_LD; ++i) lds[b_dst[i]] = rb[i];
-    __syncthreads();
+    for (int st = 0; st < NST - 1; ++st)
+        if (st < nk) SURR_ISSUE_STAGE(st, st * BK);
 
     for (int kt = 0; kt < nk; ++kt) {
-        const int st = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            const int k0 = (kt + 1) * kBK;
+        // Stage kt has landed once at most the loads of the NST-2 younger stages remain.
+        if (kt + NST - 2 < nk) wait_vmcnt<(NST - 2) * S::LOADS>();
+        else wait_vmcnt<0>();
+        __syncthreads();  // stage kt visible to all; stage kt-1 fully consumed
+        if (kt + NST - 1 < nk) SURR_ISSUE_STAGE((kt + NST - 1) % NST, (kt + NST - 1) * BK);
+        const uint4* L = lds + (kt % NST) * S::STAGE;
 #pragma unroll
-            for (int i = 0; i < S::A_LD; ++i) ra[i] = *reinterpret_cast<const uint4*>(a_src[i] + k0);
-#pragma unroll
-            for (int i = 0; i < S::B_LD; ++i) rb[i] = *reinterpret_cast<const uint4*>(b_src[i] + k0);
-        }
-        const uint4* L = lds + st * S::STAGE;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
+        for (int s = 0; s < BK / 16; ++s) {
             const int chunk = 2 * s + (lane >> 5);
             bf16x8 af[S::FM], bw[S::FN];
 #pragma unroll
             for (int i = 0; i < S::FM; ++i) {
                 const int r = wm * WM + i * 32 + (lane & 31);
-                af[i] = __builtin_bit_cast(bf16x8, L[r * 8 + (chunk ^ swz(r))]);
+                af[i] = __builtin_bit_cast(bf16x8, L[r * S::CH + (chunk ^ swz<S::CH>(r))]);
             }
 #pragma unroll
             for (int j = 0; j < S::FN; ++j) {
                 const int r = wn * WN + j * 32 + (lane & 31);
-                bw[j] = __builtin_bit_cast(bf16x8, L[(BM + r) * 8 + (chunk ^ swz(r))]);
+                bw[j] = __builtin_bit_cast(bf16x8, L[S::A_SLOTS + r * S::CH + (chunk ^ swz<S::CH>(r))]);
             }
 #pragma unroll
             for (int i = 0; i < S::FM; ++i)
@@ -125,15 +145,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restri
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw[j], af[i], acc[i][j],
                                                                         0, 0, 0);
         }
-        if (more) {
-            uint4* Ln = lds + (st ^ 1) * S::STAGE;
-#pragma unroll
-            for (int i = 0; i < S::A_LD; ++i) Ln[a_dst[i]] = ra[i];
-#pragma unroll
-            for (int i = 0; i < S::B_LD; ++i) Ln[b_dst[i]] = rb[i];
-        }
-        __syncthreads();
     }
+
+#undef SURR_ISSUE_STAGE
 
     // Lane owns row m = m0 + wm*WM + 32 i + (lane & 31) and, per 32-column fragment j,
     // columns nb + 8 q + 4 (lane >> 5) + {0..3} in acc[i][j][4 q + {0..3}].
@@ -188,11 +202,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restri
     }
 }
 
-template <int BM, int BN, int WM, int WN, Epi EPI>
+#ifndef SURR_GEMM_KERNELS_ONLY  // (kernel-only builds for standalone tuning harnesses)
+template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI>
 hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                     int M, int N, int K, hipStream_t s) {
     const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    gemm_bf16_kernel<BM, BN, WM, WN, EPI><<<(unsigned)tiles, 256, 0, s>>>(
+    gemm_bf16_kernel<BM, BN, BK, WM, WN, NST, EPI><<<(unsigned)tiles, 256, 0, s>>>(
         static_cast<const uint16_t*>(A), lda, static_cast<const uint16_t*>(B), ldb, C, ldc, M, N, K);
     return hipGetLastError();
 }
@@ -200,9 +215,11 @@ hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void
 template <Epi EPI>
 hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                          int64_t ldc, int M, int N, int K, hipStream_t s) {
-    if (M <= 128) return run_bf16<128, 128, 64, 64, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
-    return run_bf16<256, 256, 128, 128, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
+    if (M <= 128) return run_bf16<128, 128, 64, 64, 64, 2, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
+    return run_bf16<256, 256, 64, 128, 128, 2, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
 }
+
+#endif  // SURR_GEMM_KERNELS_ONLY
 
 // ---------------------------------------------------------------- fp32 FMA GEMM
 template <Epi EPI>
@@ -262,7 +279,10 @@ hipError_t run_f32(const void* A, int64_t lda, const void* B, int64_t ldb, void*
     return hipGetLastError();
 }
 
-}  // namespace
+}  // namespace gemm
+
+#ifndef SURR_GEMM_KERNELS_ONLY
+using namespace gemm;
 
 hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, int64_t ldb,
                        void* C, int64_t ldc, int M, int N, int K, hipStream_t s) {
@@ -283,5 +303,7 @@ hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, 
     }
     return hipErrorInvalidValue;
 }
+
+#endif  // SURR_GEMM_KERNELS_ONLY
 
 }  // namespace surr

@@ -429,14 +429,15 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
         SURR_HIP(done());            \
     } while (0)
 
-    auto mlp = [&](const LayerW& L, void* hin, void* uout, float* gtmp, float* xres, int M) -> surrogate_status {
+    auto mlp = [&](const LayerW& L, void* hin, void* uout, float* gtmp, float* xres, int M,
+                   int ph_gu, int ph_down) -> surrogate_status {
         if (a == Act::BF16) {
-            SURR_PHASE_RUN(SURR_PHASE_GEMM_GATE_UP, surr::launch_gemm(a, Epi::SwiGLU, hin, d, L.w_gu, d, uout, ff, M, 2 * ff, d, stream));
+            SURR_PHASE_RUN(ph_gu, surr::launch_gemm(a, Epi::SwiGLU, hin, d, L.w_gu, d, uout, ff, M, 2 * ff, d, stream));
         } else {
-            SURR_PHASE_RUN(SURR_PHASE_GEMM_GATE_UP, surr::launch_gemm(a, Epi::StoreF32, hin, d, L.w_gu, d, gtmp, 2 * ff, M, 2 * ff, d, stream));
-            SURR_PHASE_RUN(SURR_PHASE_GEMM_GATE_UP, surr::launch_swiglu_f32(gtmp, static_cast<float*>(uout), M, ff, stream));
+            SURR_PHASE_RUN(ph_gu, surr::launch_gemm(a, Epi::StoreF32, hin, d, L.w_gu, d, gtmp, 2 * ff, M, 2 * ff, d, stream));
+            SURR_PHASE_RUN(ph_gu, surr::launch_swiglu_f32(gtmp, static_cast<float*>(uout), M, ff, stream));
         }
-        SURR_PHASE_RUN(SURR_PHASE_GEMM_DOWN, surr::launch_gemm(a, Epi::ResidAddF32, uout, ff, L.w_down, ff, xres, d, M, d, ff, stream));
+        SURR_PHASE_RUN(ph_down, surr::launch_gemm(a, Epi::ResidAddF32, uout, ff, L.w_down, ff, xres, d, M, d, ff, stream));
         return SURR_OK;
     };
 
@@ -451,21 +452,21 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
             SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, o, dq, d_cu, d_work, (int)work.size(), nq, nkv, hd, stream));
             SURR_PHASE_RUN(SURR_PHASE_GEMM_O, surr::launch_gemm(a, Epi::ResidAddF32, o, dq, L.w_o, dq, x, d, Ti, d, dq, stream));
             SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x, d, nullptr, T, L.mlp_norm, d, c.rms_eps, h, d, stream));
-            const surrogate_status st = mlp(L, h, u, gu, x, Ti);
+            const surrogate_status st = mlp(L, h, u, gu, x, Ti, SURR_PHASE_GEMM_GATE_UP, SURR_PHASE_GEMM_DOWN);
             if (st != SURR_OK) return st;
         } else {
             // Only the last position of each prompt feeds the LM head: K/V above cover
             // every token; attention, O projection and MLP run for the last rows only.
             SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, o, dq, d_cu, d_work_last, batch, nq, nkv, hd, stream));
-            SURR_PHASE_RUN(SURR_PHASE_GATHER, surr::launch_gather_rows(o, dq, d_last, batch, dq, (int)m->esz, o_last, dq, stream));
-            SURR_PHASE_RUN(SURR_PHASE_GATHER, surr::launch_gather_rows(x, d, d_last, batch, d, 4, x_last, d, stream));
-            SURR_PHASE_RUN(SURR_PHASE_GEMM_O, surr::launch_gemm(a, Epi::ResidAddF32, o_last, dq, L.w_o, dq, x_last, d, batch, d, dq, stream));
-            SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, L.mlp_norm, d, c.rms_eps, h_last, d, stream));
-            const surrogate_status st = mlp(L, h_last, u_last, gu_last, x_last, batch);
+            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gather_rows(o, dq, d_last, batch, dq, (int)m->esz, o_last, dq, stream));
+            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gather_rows(x, d, d_last, batch, d, 4, x_last, d, stream));
+            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gemm(a, Epi::ResidAddF32, o_last, dq, L.w_o, dq, x_last, d, batch, d, dq, stream));
+            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, L.mlp_norm, d, c.rms_eps, h_last, d, stream));
+            const surrogate_status st = mlp(L, h_last, u_last, gu_last, x_last, batch, SURR_PHASE_LAST_ROWS, SURR_PHASE_LAST_ROWS);
             if (st != SURR_OK) return st;
         }
     }
-    SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, m->final_norm, d, c.rms_eps, y, d, stream));
+    SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, m->final_norm, d, c.rms_eps, y, d, stream));
     SURR_PHASE_RUN(SURR_PHASE_LM_HEAD, surr::launch_gemm(a, Epi::StoreF32, y, d, m->lm_head, d, logits, c.vocab, batch, c.vocab, d, stream));
     SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_verdict(logits, c.vocab, batch, c.vocab, d_vid, n_verdict, logprobs_d, probs_d, confidence_d, verdict_d, stream));
 #undef SURR_PHASE_RUN

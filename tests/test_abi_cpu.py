@@ -85,3 +85,12 @@ def test_status_strings():
     for s in range(0, -8, -1):
         assert L.surrogate_status_string(s)
     assert L.surrogate_status_string(-3) == b"token id out of range"
+
+
+def test_library_has_no_unresolved_kernel_stubs():
+    # a kernel template dropped by the host compilation pass leaves an undefined launch
+    # stub that only fails when that kernel is first launched
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--undefined-only", B.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    assert "__device_stub__" not in out
