@@ -32,8 +32,9 @@ struct Tile {
 
 // Chunk order inside an LDS row: XOR with row bits so 16 consecutive rows read at one
 // logical chunk land on 16 distinct 16-byte bank groups.
-template <int CH>
+template <int CH, int SWZ = 0>
 __device__ __forceinline__ int swz(int row) {
+    if constexpr (SWZ == 1) return row & (CH - 1);
     if constexpr (CH == 8) return (row >> 1) & 7;
     else return (row >> 2) & 3;
 }
@@ -49,8 +50,45 @@ __device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); 
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
+// Byte offset of a __shared__ object inside the workgroup's LDS allocation.
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+    return (uint32_t)(uintptr_t)(lds_ptr_t)p;
+}
 
-template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI>
+// 16 bytes per lane from global memory straight into LDS at lds_addr + 16 * lane
+// (lds_addr is wave-uniform and goes through M0).  Written as inline assembly so the
+// compiler's wait-count model, which treats LDS DMA conservatively and would force a
+// full LDS-read drain before every MFMA group, does not see it: the kernel orders these
+// loads itself (explicit vmcnt waits and a barrier before any LDS read of the stage).
+__device__ __forceinline__ void dma_load_16B(const void* gptr, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+                 : "memory", "m0");
+}
+
+
+// Tile order.  The hardware hands workgroup i to XCD i % 8, and each XCD has its own
+// L2.  With XCD remapping, XCD x receives the contiguous virtual range
+// [x * per_xcd, (x + 1) * per_xcd); virtual ids then walk GROUP M-tiles down before
+// moving one N-tile right, so the ~32 tiles resident on one XCD form a compact
+// GROUP x (32 / GROUP) block that shares A and B slabs in that XCD's L2.
+template <int GROUP, bool XCD>
+__device__ __forceinline__ void tile_coords(int pid, int tiles_m, int tiles_n, int* tm, int* tn) {
+    if constexpr (XCD) {
+        const int total = tiles_m * tiles_n;
+        const int per_xcd = total / 8;
+        if (pid < per_xcd * 8) pid = (pid % 8) * per_xcd + pid / 8;
+    }
+    const int width = GROUP * tiles_n;
+    const int first_m = (pid / width) * GROUP;
+    const int gsz = min(tiles_m - first_m, GROUP);
+    *tm = first_m + (pid % width) % gsz;
+    *tn = (pid % width) / gsz;
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI, int GROUP = 8, bool XCD = false,
+          int SWZ = 0>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restrict__ A,
                                                         int64_t lda,
                                                         const uint16_t* __restrict__ B,
@@ -61,50 +99,45 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restri
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / S::WAVES_N, wn = wave % S::WAVES_N;
 
-    // Grouped tile order: GROUP consecutive M tiles sweep N together so the A rows they
-    // share stay in L2.
-    constexpr int GROUP = 8;
     const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-    const int pid = blockIdx.x;
-    const int width = GROUP * tiles_n;
-    const int first_m = (pid / width) * GROUP;
-    const int gsz = min(tiles_m - first_m, GROUP);
-    const int tm = first_m + (pid % width) % gsz;
-    const int tn = (pid % width) / gsz;
+    int tm, tn;
+    tile_coords<GROUP, XCD>(blockIdx.x, tiles_m, tiles_n, &tm, &tn);
     const int m0 = tm * BM, n0 = tn * BN;
 
     // Direct-to-LDS loads: wavefront `wave`, load j fills the 64 consecutive slots
     // (wave * LOADS + j) * 64 + lane of a stage (the hardware places lane l's 16 bytes at
     // slot base + l).  Slot -> (row, physical chunk) -> logical chunk via the swizzle;
-    // rows past M or N are clamped (their results are never stored).
-    const uint16_t* gsrc[S::LOADS];
+    // rows past M or N are clamped (their results are never stored).  Each load reads
+    // either the A tile or the B tile (uniform per wavefront and load), so a thread keeps
+    // only a 32-bit byte offset per load against the tile's base pointer.
+    const char* a_tile = reinterpret_cast<const char*>(A + (int64_t)m0 * lda);
+    const char* b_tile = reinterpret_cast<const char*>(B + (int64_t)n0 * ldb);
+    uint32_t goff[S::LOADS];
+    const uint32_t lds_base = lds_offset(lds);
 #pragma unroll
     for (int j = 0; j < S::LOADS; ++j) {
         const int slot = (wave * S::LOADS + j) * 64 + lane;
         if (slot < S::A_SLOTS) {
-            const int r = slot / S::CH, c = (slot % S::CH) ^ swz<S::CH>(r);
-            gsrc[j] = A + (int64_t)min(m0 + r, M - 1) * lda + c * 8;
+            const int r = slot / S::CH, c = (slot % S::CH) ^ swz<S::CH, SWZ>(r);
+            goff[j] = (uint32_t)(((int64_t)(min(m0 + r, M - 1) - m0) * lda + c * 8) * 2);
         } else {
             const int sb = slot - S::A_SLOTS;
-            const int r = sb / S::CH, c = (sb % S::CH) ^ swz<S::CH>(r);
-            gsrc[j] = B + (int64_t)min(n0 + r, N - 1) * ldb + c * 8;
+            const int r = sb / S::CH, c = (sb % S::CH) ^ swz<S::CH, SWZ>(r);
+            goff[j] = (uint32_t)(((int64_t)(min(n0 + r, N - 1) - n0) * ldb + c * 8) * 2);
         }
     }
+    // Source of load j of this thread for the stage starting at column k0.
+#define SURR_DMA_SRC(j, k0)                                                                  \
+    ((((wave * S::LOADS + (j)) * 64) < S::A_SLOTS ? a_tile : b_tile) + 2 * (int64_t)(k0) + goff[j])
 
-    // One stage of direct-to-LDS loads (load j of wavefront `wave` fills the 64 slots
-    // starting at (wave * LOADS + j) * 64).  The builtin exists only in the device pass;
-    // the host pass compiles an empty body (it never runs kernel code).
-#if defined(__HIP_DEVICE_COMPILE__)
-#define SURR_ISSUE_STAGE(stage, k0)                                                          \
-    do {                                                                                     \
-        _Pragma("unroll") for (int j = 0; j < S::LOADS; ++j)                                 \
-            __builtin_amdgcn_global_load_lds(                                                \
-                gsrc[j] + (k0),                                                              \
-                (lds_ptr_t)(lds + (stage) * S::STAGE + (wave * S::LOADS + j) * 64), 16, 0, 0); \
+    // One stage of direct-to-LDS loads: load j of wavefront `wave` fills the 64 slots
+    // starting at (wave * LOADS + j) * 64.
+#define SURR_ISSUE_STAGE(stage, k0)                                                              \
+    do {                                                                                         \
+        _Pragma("unroll") for (int j = 0; j < S::LOADS; ++j)                                     \
+            dma_load_16B(SURR_DMA_SRC(j, k0), lds_base + (uint32_t)((((stage) * S::STAGE) +      \
+                                                                (wave * S::LOADS + j) * 64) * 16)); \
     } while (0)
-#else
-#define SURR_ISSUE_STAGE(stage, k0) ((void)(stage), (void)(k0))
-#endif
 
     f32x16 acc[S::FM][S::FN];
 #pragma unroll
@@ -112,42 +145,105 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restri
 #pragma unroll
         for (int j = 0; j < S::FN; ++j) acc[i][j] = f32x16{};
 
-    const int nk = K / BK;
+    // Fragment reads for MFMA step s of the stage at L.
+    auto read_a = [&](const uint4* L, int s, bf16x8 (&af)[S::FM]) {
+        const int chunk = 2 * s + (lane >> 5);
 #pragma unroll
-    for (int st = 0; st < NST - 1; ++st)
-        if (st < nk) SURR_ISSUE_STAGE(st, st * BK);
+        for (int i = 0; i < S::FM; ++i) {
+            const int r = wm * WM + i * 32 + (lane & 31);
+            af[i] = __builtin_bit_cast(bf16x8, L[r * S::CH + (chunk ^ swz<S::CH, SWZ>(r))]);
+        }
+    };
+    auto read_b = [&](const uint4* L, int s, bf16x8 (&bw)[S::FN]) {
+        const int chunk = 2 * s + (lane >> 5);
+#pragma unroll
+        for (int j = 0; j < S::FN; ++j) {
+            const int r = wn * WN + j * 32 + (lane & 31);
+            bw[j] = __builtin_bit_cast(bf16x8, L[S::A_SLOTS + r * S::CH + (chunk ^ swz<S::CH, SWZ>(r))]);
+        }
+    };
+    // MFMAs of fragment rows [i0, i1) for the fragments in buffer cb.
+#define SURR_MFMA_ROWS(cb, i0, i1)                                                            \
+    _Pragma("unroll") for (int mi_ = (i0); mi_ < (i1); ++mi_)                                 \
+        _Pragma("unroll") for (int mj_ = 0; mj_ < S::FN; ++mj_)                               \
+            acc[mi_][mj_] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cb][mj_], fa[cb][mi_], \
+                                                                    acc[mi_][mj_], 0, 0, 0)
+
+    // Software pipeline.  Stage ring of NST buffers; the fragments of MFMA step s+1 are
+    // read while the MFMAs of step s run.  With NST >= 3, the DMA of stage kt+NST-1 is
+    // spread between the MFMAs of the first step of stage kt (its buffer was released by
+    // the barrier that opened stage kt), keeping NST-1 stages in flight without stalling
+    // MFMA issue.  With NST == 2 the refill has to wait for that barrier instead.  The
+    // last step of a stage waits for the next stage (vmcnt), passes the barrier and reads
+    // the next stage's first fragments.  sched_barrier pins this order.
+    constexpr int KSTEPS = BK / 16;
+    constexpr int FH = S::FM / 2;
+    static_assert(KSTEPS % 2 == 0 && S::FM % 2 == 0, "fragment double buffer");
+    const int nk = K / BK;
+    // Stage loads past the end of K re-load the last stage (always in bounds) into a
+    // buffer that is never read again; this keeps the loop free of branches, which the
+    // register allocator needs to keep all accumulators resident.
+#pragma unroll
+    for (int st = 0; st < NST - 1; ++st) SURR_ISSUE_STAGE(st, min(st, nk - 1) * BK);
+    wait_vmcnt<(NST - 2) * S::LOADS>();
+    __syncthreads();
+    if (NST == 2) SURR_ISSUE_STAGE(1, min(1, nk - 1) * BK);
+    bf16x8 fa[2][S::FM], fb[2][S::FN];
+    read_a(lds, 0, fa[0]);
+    read_b(lds, 0, fb[0]);
 
     for (int kt = 0; kt < nk; ++kt) {
-        // Stage kt has landed once at most the loads of the NST-2 younger stages remain.
-        if (kt + NST - 2 < nk) wait_vmcnt<(NST - 2) * S::LOADS>();
-        else wait_vmcnt<0>();
-        __syncthreads();  // stage kt visible to all; stage kt-1 fully consumed
-        if (kt + NST - 1 < nk) SURR_ISSUE_STAGE((kt + NST - 1) % NST, (kt + NST - 1) * BK);
         const uint4* L = lds + (kt % NST) * S::STAGE;
 #pragma unroll
-        for (int s = 0; s < BK / 16; ++s) {
-            const int chunk = 2 * s + (lane >> 5);
-            bf16x8 af[S::FM], bw[S::FN];
+        for (int s = 0; s < KSTEPS; ++s) {
+            const int cb = s & 1;
+            if (s + 1 < KSTEPS) {
+                read_b(L, s + 1, fb[cb ^ 1]);
+                read_a(L, s + 1, fa[cb ^ 1]);
+                __builtin_amdgcn_sched_barrier(0);
+                if (NST >= 3 && s == 0) {
+                    const int rs = (kt + NST - 1) % NST, rk = min(kt + NST - 1, nk - 1) * BK;
+                    constexpr int PER_ROW = NST >= 3 ? S::LOADS / S::FM : 1;
+                    static_assert(NST == 2 || S::LOADS % S::FM == 0, "DMA interleave per row");
 #pragma unroll
-            for (int i = 0; i < S::FM; ++i) {
-                const int r = wm * WM + i * 32 + (lane & 31);
-                af[i] = __builtin_bit_cast(bf16x8, L[r * S::CH + (chunk ^ swz<S::CH>(r))]);
+                    for (int row = 0; row < S::FM; ++row) {
+                        SURR_MFMA_ROWS(cb, row, row + 1);
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int q = 0; q < PER_ROW; ++q) {
+                            const int jj = row * PER_ROW + q;
+                            dma_load_16B(SURR_DMA_SRC(jj, rk),
+                                         lds_base + (uint32_t)((rs * S::STAGE + (wave * S::LOADS + jj) * 64) * 16));
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                } else {
+                    SURR_MFMA_ROWS(cb, 0, S::FM);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            } else {
+                SURR_MFMA_ROWS(cb, 0, FH);
+                __builtin_amdgcn_sched_barrier(0);
+                // every wave's reads of stage kt are done before anyone refills it; then
+                // stage kt+1 (issued NST-1 stages ago) must have landed
+                __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));  // lgkmcnt(0)
+                wait_vmcnt<(NST - 2) * S::LOADS>();
+                __syncthreads();
+                if (NST == 2) SURR_ISSUE_STAGE(kt % 2, min(kt + 2, nk - 1) * BK);
+                const uint4* Ln = lds + ((kt + 1) % NST) * S::STAGE;
+                read_a(Ln, 0, fa[cb ^ 1]);
+                read_b(Ln, 0, fb[cb ^ 1]);
+                __builtin_amdgcn_sched_barrier(0);
+                SURR_MFMA_ROWS(cb, FH, S::FM);
+                __builtin_amdgcn_sched_barrier(0);
             }
-#pragma unroll
-            for (int j = 0; j < S::FN; ++j) {
-                const int r = wn * WN + j * 32 + (lane & 31);
-                bw[j] = __builtin_bit_cast(bf16x8, L[S::A_SLOTS + r * S::CH + (chunk ^ swz<S::CH>(r))]);
-            }
-#pragma unroll
-            for (int i = 0; i < S::FM; ++i)
-#pragma unroll
-                for (int j = 0; j < S::FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bw[j], af[i], acc[i][j],
-                                                                        0, 0, 0);
         }
     }
+    wait_vmcnt<0>();  // no DMA may still target LDS when the workgroup retires
+#undef SURR_MFMA_ROWS
 
 #undef SURR_ISSUE_STAGE
+#undef SURR_DMA_SRC
 
     // Lane owns row m = m0 + wm*WM + 32 i + (lane & 31) and, per 32-column fragment j,
     // columns nb + 8 q + 4 (lane >> 5) + {0..3} in acc[i][j][4 q + {0..3}].
@@ -207,16 +303,19 @@ template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI>
 hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                     int M, int N, int K, hipStream_t s) {
     const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    gemm_bf16_kernel<BM, BN, BK, WM, WN, NST, EPI><<<(unsigned)tiles, 256, 0, s>>>(
+    gemm_bf16_kernel<BM, BN, BK, WM, WN, NST, EPI, 8, true><<<(unsigned)tiles, 256, 0, s>>>(
         static_cast<const uint16_t*>(A), lda, static_cast<const uint16_t*>(B), ldb, C, ldc, M, N, K);
     return hipGetLastError();
 }
 
+// Tile choice (measured on the 7B projection shapes): 256 x 256 x 32 tiles with a
+// 4-stage ring and XCD-grouped order; 128 x 128 tiles for the few-row GEMMs of the
+// last-position head and the pruned final layer.
 template <Epi EPI>
 hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                          int64_t ldc, int M, int N, int K, hipStream_t s) {
-    if (M <= 128) return run_bf16<128, 128, 64, 64, 64, 2, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
-    return run_bf16<256, 256, 64, 128, 128, 2, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
+    if (M <= 128) return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
+    return run_bf16<256, 256, 32, 128, 128, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
 }
 
 #endif  // SURR_GEMM_KERNELS_ONLY
