@@ -80,6 +80,24 @@ def cpu_baseline(shape, W, tok, L, vid) -> dict:
             "cpu": platform.processor() or platform.machine()}
 
 
+TRAFFIC_REPORT = os.path.join(ROOT, "profiles", "gemm_gate_up_{config}_traffic.md")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2605_31464_amd", "csrc", "k_gemm.hip")
+
+
+def measured_traffic(config: str):
+    """HBM bytes per launch of the gate/up GEMM from the committed rocprofv3 counter
+    report, or None when there is none or the GEMM source changed since it was taken."""
+    from paper_2605_31464_amd.rocprof_summary import source_sha256
+    path = TRAFFIC_REPORT.format(config=config)
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        if line.startswith("bench-traffic:"):
+            _, val, sha = line.split()
+            return float(val) if sha == source_sha256(GEMM_SOURCE) else None
+    return None
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -89,6 +107,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the per-phase HIP-event timing (the roofline block)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run one device-to-device copy of this size first (reference "
+                         "dispatch for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -132,6 +153,14 @@ def main() -> int:
     stream = torch.cuda.current_stream()
     print(f"[bench] {w.name}: B={B_} T={T} setup {time.perf_counter() - t_setup:.1f}s",
           file=sys.stderr, flush=True)
+
+    if args.copy_calibration_mib:
+        src = torch.ones(args.copy_calibration_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step():
         B.surrogate_score_pairs(model, tok, L, vid, ws, lp, conf, p, verdict, stream=stream)
@@ -194,7 +223,8 @@ def main() -> int:
             out["roofline"] = {"kernel": "gemm_bf16 SwiGLU epilogue (gate/up projection)",
                                "bound": "mfma", "achieved": ach / 1e12,
                                "peak": PEAK_BF16 / 1e12, "unit": "TFLOP/s",
-                               "frac": ach / PEAK_BF16, "traffic": None,
+                               "frac": ach / PEAK_BF16,
+                               "traffic": measured_traffic(args.config),
                                "avg_launch_ms": avg_s * 1e3, "launches": n}
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on a bounded sample", file=sys.stderr, flush=True)
