@@ -93,7 +93,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restri
                                                         int64_t lda,
                                                         const uint16_t* __restrict__ B,
                                                         int64_t ldb, void* __restrict__ C,
-                                                        int64_t ldc, int M, int N, int K) {
+                                                        int64_t ldc, int M, int N, int K,
+                                                        RopeArgs rope) {
     using S = Tile<BM, BN, BK, WM, WN, NST>;
     __shared__ uint4 lds[NST * S::STAGE];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -271,6 +272,53 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restri
                     *reinterpret_cast<uint2*>(out + 8 * q + 4 * h) = o;
                 }
             }
+        } else if constexpr (EPI == Epi::StoreActRope) {
+            // Rotate-half RoPE on whole heads inside this wavefront's columns: the pair
+            // (i, i + hd/2) sits in fragments (j, j + hd/64) at the same lane position.
+            static_assert(WN % 128 == 0, "wave tile must hold whole 128-dim heads");
+            const int hd = rope.head_dim, half = hd >> 1, fstep = hd / 64;
+            const int pos = rope.pos[m];
+            const float2* cs = rope.cs + (int64_t)pos * half;
+            uint16_t* out = static_cast<uint16_t*>(C) + (int64_t)m * ldc;
+#pragma unroll
+            for (int j = 0; j < S::FN; ++j) {
+                const int nb = n0 + wn * WN + j * 32;
+                if (nb >= N) continue;
+                const bool rotated = nb < rope.cols;
+                const bool first_half = ((nb % hd) < half);
+                if (rotated && !first_half) continue;  // written together with its partner
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int n = nb + 8 * q + 4 * h;
+                    float v[4], w[4];
+                    if (rotated) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            // partner fragment index: j + fstep (fstep = 1 for hd 64, 2 for hd 128)
+                            const float x1 = acc[i][j][4 * q + e];
+                            const float x2 = fstep == 1 ? acc[i][(j + 1) % S::FN][4 * q + e]
+                                                        : acc[i][(j + 2) % S::FN][4 * q + e];
+                            const float2 c = cs[(n + e) % hd];
+                            v[e] = x1 * c.x - x2 * c.y;
+                            w[e] = x2 * c.x + x1 * c.y;
+                        }
+                        uint2 o1, o2;
+                        o1.x = pack_bf16x2(v[0], v[1]);
+                        o1.y = pack_bf16x2(v[2], v[3]);
+                        o2.x = pack_bf16x2(w[0], w[1]);
+                        o2.y = pack_bf16x2(w[2], w[3]);
+                        *reinterpret_cast<uint2*>(out + n) = o1;
+                        *reinterpret_cast<uint2*>(out + n + half) = o2;
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
+                        uint2 o1;
+                        o1.x = pack_bf16x2(v[0], v[1]);
+                        o1.y = pack_bf16x2(v[2], v[3]);
+                        *reinterpret_cast<uint2*>(out + n) = o1;
+                    }
+                }
+            }
         } else {
 #pragma unroll
             for (int j = 0; j < S::FN; ++j) {
@@ -301,10 +349,11 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restri
 #ifndef SURR_GEMM_KERNELS_ONLY  // (kernel-only builds for standalone tuning harnesses)
 template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI>
 hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
-                    int M, int N, int K, hipStream_t s) {
+                    int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
     const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
     gemm_bf16_kernel<BM, BN, BK, WM, WN, NST, EPI, 8, true><<<(unsigned)tiles, 256, 0, s>>>(
-        static_cast<const uint16_t*>(A), lda, static_cast<const uint16_t*>(B), ldb, C, ldc, M, N, K);
+        static_cast<const uint16_t*>(A), lda, static_cast<const uint16_t*>(B), ldb, C, ldc, M, N, K,
+        rope);
     return hipGetLastError();
 }
 
@@ -313,9 +362,12 @@ hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void
 // last-position head and the pruned final layer.
 template <Epi EPI>
 hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
-                         int64_t ldc, int M, int N, int K, hipStream_t s) {
-    if (M <= 128) return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
-    return run_bf16<256, 256, 32, 128, 128, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s);
+                         int64_t ldc, int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
+    if constexpr (EPI != Epi::StoreActRope) {  // RoPE needs a wave tile of whole heads
+        if (M <= 128)
+            return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+    }
+    return run_bf16<256, 256, 32, 128, 128, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
 }
 
 #endif  // SURR_GEMM_KERNELS_ONLY
@@ -384,7 +436,8 @@ hipError_t run_f32(const void* A, int64_t lda, const void* B, int64_t ldb, void*
 using namespace gemm;
 
 hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, int64_t ldb,
-                       void* C, int64_t ldc, int M, int N, int K, hipStream_t s) {
+                       void* C, int64_t ldc, int M, int N, int K, hipStream_t s,
+                       const RopeArgs& rope) {
     if (M <= 0 || N <= 0) return hipSuccess;
     if (t == Act::F32) {
         switch (e) {
@@ -395,10 +448,13 @@ hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, 
         }
     }
     switch (e) {
-        case Epi::StoreAct: return dispatch_bf16<Epi::StoreAct>(A, lda, B, ldb, C, ldc, M, N, K, s);
-        case Epi::ResidAddF32: return dispatch_bf16<Epi::ResidAddF32>(A, lda, B, ldb, C, ldc, M, N, K, s);
-        case Epi::SwiGLU: return dispatch_bf16<Epi::SwiGLU>(A, lda, B, ldb, C, ldc, M, N, K, s);
-        case Epi::StoreF32: return dispatch_bf16<Epi::StoreF32>(A, lda, B, ldb, C, ldc, M, N, K, s);
+        case Epi::StoreAct: return dispatch_bf16<Epi::StoreAct>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        case Epi::ResidAddF32: return dispatch_bf16<Epi::ResidAddF32>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        case Epi::SwiGLU: return dispatch_bf16<Epi::SwiGLU>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        case Epi::StoreF32: return dispatch_bf16<Epi::StoreF32>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        case Epi::StoreActRope:
+            if (rope.head_dim != 64 && rope.head_dim != 128) return hipErrorInvalidValue;
+            return dispatch_bf16<Epi::StoreActRope>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
     }
     return hipErrorInvalidValue;
 }

@@ -45,15 +45,27 @@ hipError_t launch_select(const float* conf, int n, int mode, float tau, int k, i
                          hipStream_t s);
 
 // ---- k_gemm.hip
-enum class Epi { StoreAct, ResidAddF32, SwiGLU, StoreF32 };
+enum class Epi { StoreAct, ResidAddF32, SwiGLU, StoreF32, StoreActRope };
+
+// Rotary embedding applied inside the GEMM epilogue (Epi::StoreActRope): columns
+// [0, cols) hold whole heads of head_dim; within each head, columns i and i + hd/2 of
+// row m rotate by the angle of position pos[m] (table cs[pos][i] = (cos, sin)).
+struct RopeArgs {
+    const int32_t* pos = nullptr;
+    const float2* cs = nullptr;
+    int cols = 0;
+    int head_dim = 0;
+};
 
 // C = A[M,K] * B[N,K]^T (both K-contiguous), fp32 accumulation, fused epilogue:
 //   StoreAct    C (activation type) [M, N]
 //   ResidAddF32 C (fp32) += result
 //   SwiGLU      B rows interleave gate/up in 32-row blocks; C[M, N/2] = silu(g) * u
 //   StoreF32    C (fp32) [M, N]
+//   StoreActRope  as StoreAct, with RoPE applied first (bf16 only)
 hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, int64_t ldb,
-                       void* C, int64_t ldc, int M, int N, int K, hipStream_t s);
+                       void* C, int64_t ldc, int M, int N, int K, hipStream_t s,
+                       const RopeArgs& rope = RopeArgs());
 
 // ---- k_attention.hip
 // Causal GQA attention over the packed qkv rows.  work[i] = (prompt, q_tile) items;

@@ -96,6 +96,7 @@ struct surrogate_model {
     surrogate_config cfg{};
     Act act = Act::BF16;
     size_t esz = 2;
+
     char* arena = nullptr;
     void* embed = nullptr;
     void* lm_head = nullptr;
@@ -404,6 +405,7 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
     const int dq = (int)m->d_q(), dqkv = (int)m->d_qkv();
     const int Ti = (int)T;
 
+
     // Phase bracketing for the measurement hook (a no-op unless profiling is on).
     auto mark = [&](int phase) -> hipError_t {
         if (!m->profiling) return hipSuccess;
@@ -446,8 +448,18 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
         const LayerW& L = m->layers[l];
         const bool final_layer = l == c.n_layers - 1;
         SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x, d, nullptr, T, L.attn_norm, d, c.rms_eps, h, d, stream));
-        SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreAct, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream));
-        SURR_PHASE_RUN(SURR_PHASE_ROPE, surr::launch_rope(a, qkv, dqkv, T, d_pos, nq + nkv, hd, m->rope_cs, stream));
+        if (a == Act::BF16) {
+            // RoPE on the q and k heads happens in the GEMM epilogue (one rounding)
+            surr::RopeArgs rope;
+            rope.pos = d_pos;
+            rope.cs = m->rope_cs;
+            rope.cols = (nq + nkv) * hd;
+            rope.head_dim = hd;
+            SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream, rope));
+        } else {
+            SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreAct, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream));
+            SURR_PHASE_RUN(SURR_PHASE_ROPE, surr::launch_rope(a, qkv, dqkv, T, d_pos, nq + nkv, hd, m->rope_cs, stream));
+        }
         if (!final_layer) {
             SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, o, dq, d_cu, d_work, (int)work.size(), nq, nkv, hd, stream));
             SURR_PHASE_RUN(SURR_PHASE_GEMM_O, surr::launch_gemm(a, Epi::ResidAddF32, o, dq, L.w_o, dq, x, d, Ti, d, dq, stream));

@@ -1,0 +1,71 @@
+"""GPU parity at the benchmark's full sizes.
+
+The whole batch of a config is scored on the GPU exactly as bench.py does (one
+surrogate_score_pairs call over all prompts); the float64 oracle recomputes sampled
+prompts one by one (the shortest prompt and prompt 0), and the deferral step is checked
+bit-exactly on the GPU's own confidence vector.  Shapes the oracle cannot finish at full
+depth (14B) are checked at their full width with fewer layers.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import select as osel
+from oracle import transformer as ot
+from paper_2605_31464_amd import binding as B
+from paper_2605_31464_amd import synth
+
+from conftest import arch_of
+from test_gpu_parity import TOL, assert_parity, make_scorer, padded, rng_prompts
+
+pytestmark = pytest.mark.gpu
+
+
+def score_full_config(name, rows):
+    w = synth.CONFIGS[name]
+    scorer, W = make_scorer(w.shape)
+    tok, L = synth.make_prompts(w)
+    vid = synth.verdict_ids(w)
+    out = scorer.score(tok, L, vid)
+    assert B.surrogate_device_status(scorer.model) == B.SURR_OK
+    rows = [int(np.argmin(L)) if r == "shortest" else r for r in rows]
+    ref = ot.score(arch_of(w.shape), W, [tok[i, : L[i]] for i in rows], vid)
+    assert_parity(out, ref, TOL["bf16"], rows)
+    conf = out["confidence"]
+    if w.select[0] == "budget":
+        d, a, c = B.surrogate_select(conf, B.SURR_SELECT_BUDGET, budget_k=w.budget_k)
+        rd, ra = osel.select_budget(conf.cpu().numpy(), w.budget_k)
+    else:
+        d, a, c = B.surrogate_select(conf, B.SURR_SELECT_THRESHOLD, threshold=w.select[1])
+        rd, ra = osel.select_threshold(conf.cpu().numpy(), w.select[1])
+    c = c.cpu().numpy()
+    assert np.array_equal(d.cpu().numpy()[: c[0]], rd)
+    assert np.array_equal(a.cpu().numpy()[: c[1]], ra)
+    return scorer, out, tok, L, vid
+
+
+@pytest.mark.timeout(900)
+def test_7b_config_full_batch_sampled_prompt():
+    scorer, out, tok, L, vid = score_full_config("7b", ["shortest"])
+    # the sampled prompt scored alone gives bitwise the same result as inside the batch
+    i = int(np.argmin(L))
+    t1, l1 = padded([tok[i, : L[i]]])
+    alone = scorer.score(t1, l1, vid)
+    assert torch.equal(alone["logprobs"][0], out["logprobs"][i])
+
+
+@pytest.mark.timeout(600)
+def test_1p5b_config_full_batch_sampled_prompts():
+    score_full_config("1p5b", ["shortest", 0])
+
+
+@pytest.mark.timeout(600)
+def test_14b_shape_full_width_reduced_depth():
+    shape = synth.CONFIGS["14b"].shape.replace(n_layers=2)
+    scorer, W = make_scorer(shape, gain_std=0.1)
+    lengths = [1, 127, 300, 1100]
+    tok, L = padded(rng_prompts(shape.vocab, lengths, 21))
+    vid = list(range(shape.vocab - 5, shape.vocab))
+    out = scorer.score(tok, L, vid)
+    assert_parity(out, ot.score(arch_of(shape), W, [tok[i, : L[i]] for i in range(len(L))], vid),
+                  TOL["bf16"])

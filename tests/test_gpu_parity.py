@@ -42,16 +42,20 @@ def oracle_for(shape, W, tok, L, vid, rows=None):
     return ot.score(arch_of(shape), W, [tok[i, : L[i]] for i in rows], vid)
 
 
-def assert_parity(out, ref, tol, rows=None):
+def assert_parity(out, ref, tol, rows=None, lp_tol=None):
+    """tol bounds p and q; lp_tol (default tol) bounds the full-vocabulary log-probs."""
     rows = slice(None) if rows is None else list(rows)
+    lp_tol = tol if lp_tol is None else lp_tol
     lp = out["logprobs"].cpu().numpy()[rows]
     p = out["p"].cpu().numpy()[rows]
     q = out["confidence"].cpu().numpy()[rows]
     v = out["verdict"].cpu().numpy()[rows]
     err = np.abs(lp - ref["logprobs"]).max()
-    print(f"max |lp - oracle| = {err:.3e} (tol {tol})", flush=True)
-    assert err <= tol
-    assert np.abs(p - ref["p"]).max() <= tol
+    perr = np.abs(p - ref["p"]).max()
+    print(f"max |lp - oracle| = {err:.3e} (tol {lp_tol}), max |p - oracle| = {perr:.3e} "
+          f"(tol {tol})", flush=True)
+    assert err <= lp_tol
+    assert perr <= tol
     assert np.abs(q - ref["confidence"]).max() <= tol
     sure = ref["margin"] > 0.1
     assert np.array_equal(v[sure], ref["verdict"][sure])
