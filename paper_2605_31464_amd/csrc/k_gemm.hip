@@ -20,13 +20,15 @@ namespace gemm {
 template <int BM, int BN, int BK, int WM, int WN, int NST>
 struct Tile {
     static constexpr int WAVES_N = BN / WN;
-    static_assert((BM / WM) * (BN / WN) == 4, "four wavefronts per workgroup");
+    static constexpr int NW = (BM / WM) * (BN / WN);  // wavefronts per workgroup
+    static constexpr int THREADS = 64 * NW;
+    static_assert(NW == 4 || NW == 8 || NW == 16, "4, 8 or 16 wavefronts per workgroup");
     static constexpr int FM = WM / 32, FN = WN / 32;
     static constexpr int CH = BK / 8;               // 16-byte chunks per tile row
     static constexpr int A_SLOTS = BM * CH, B_SLOTS = BN * CH;
     static constexpr int STAGE = A_SLOTS + B_SLOTS;  // 16-byte LDS slots per stage
-    static constexpr int LOADS = STAGE / 256;        // DMA loads per thread per stage
-    static_assert(A_SLOTS % 64 == 0 && STAGE % 256 == 0, "whole wavefront loads");
+    static constexpr int LOADS = STAGE / THREADS;    // DMA loads per thread per stage
+    static_assert(A_SLOTS % 64 == 0 && STAGE % THREADS == 0, "whole wavefront loads");
     static_assert(NST >= 2 && (NST - 2) * LOADS <= 63, "vmcnt range");
 };
 
@@ -88,8 +90,8 @@ __device__ __forceinline__ void tile_coords(int pid, int tiles_m, int tiles_n, i
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI, int GROUP = 8, bool XCD = false,
-          int SWZ = 0>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restrict__ A,
+          int SWZ = 0, int MINB = 1>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_kernel(const uint16_t* __restrict__ A,
                                                         int64_t lda,
                                                         const uint16_t* __restrict__ B,
                                                         int64_t ldb, void* __restrict__ C,
@@ -204,15 +206,13 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(const uint16_t* __restri
                 __builtin_amdgcn_sched_barrier(0);
                 if (NST >= 3 && s == 0) {
                     const int rs = (kt + NST - 1) % NST, rk = min(kt + NST - 1, nk - 1) * BK;
-                    constexpr int PER_ROW = NST >= 3 ? S::LOADS / S::FM : 1;
-                    static_assert(NST == 2 || S::LOADS % S::FM == 0, "DMA interleave per row");
 #pragma unroll
                     for (int row = 0; row < S::FM; ++row) {
                         SURR_MFMA_ROWS(cb, row, row + 1);
                         __builtin_amdgcn_sched_barrier(0);
+                        // loads [row * LOADS / FM, (row + 1) * LOADS / FM) after MFMA row `row`
 #pragma unroll
-                        for (int q = 0; q < PER_ROW; ++q) {
-                            const int jj = row * PER_ROW + q;
+                        for (int jj = row * S::LOADS / S::FM; jj < (row + 1) * S::LOADS / S::FM; ++jj) {
                             dma_load_16B(SURR_DMA_SRC(jj, rk),
                                          lds_base + (uint32_t)((rs * S::STAGE + (wave * S::LOADS + jj) * 64) * 16));
                         }
@@ -351,23 +351,27 @@ template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI>
 hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                     int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
     const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    gemm_bf16_kernel<BM, BN, BK, WM, WN, NST, EPI, 8, true><<<(unsigned)tiles, 256, 0, s>>>(
+    gemm_bf16_kernel<BM, BN, BK, WM, WN, NST, EPI, 8, true><<<(unsigned)tiles, Tile<BM, BN, BK, WM, WN, NST>::THREADS, 0, s>>>(
         static_cast<const uint16_t*>(A), lda, static_cast<const uint16_t*>(B), ldb, C, ldc, M, N, K,
         rope);
     return hipGetLastError();
 }
 
-// Tile choice (measured on the 7B projection shapes): 256 x 256 x 32 tiles with a
-// 4-stage ring and XCD-grouped order; 128 x 128 tiles for the few-row GEMMs of the
-// last-position head and the pruned final layer.
+// Tile choice (measured on the 7B projection shapes): 256 x 256 x 32 tiles, eight
+// wavefronts of 128 x 64 (two per SIMD, so one hides the other's waits), a 3-stage ring
+// and XCD-grouped order; 128 x 128 tiles for the few-row GEMMs of the last-position
+// head and the pruned final layer.  The RoPE epilogue keeps four wavefronts of 128 x 128
+// so that each wavefront holds whole 128-wide heads.
 template <Epi EPI>
 hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                          int64_t ldc, int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
-    if constexpr (EPI != Epi::StoreActRope) {  // RoPE needs a wave tile of whole heads
+    if constexpr (EPI == Epi::StoreActRope) {  // RoPE needs a wave tile of whole heads
+        return run_bf16<256, 256, 32, 128, 128, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+    } else {
         if (M <= 128)
             return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        return run_bf16<256, 256, 32, 128, 64, 3, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
     }
-    return run_bf16<256, 256, 32, 128, 128, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
 }
 
 #endif  // SURR_GEMM_KERNELS_ONLY
