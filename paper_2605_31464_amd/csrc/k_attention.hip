@@ -2,13 +2,25 @@
 //
 // bf16 path (v_mfma_f32_32x32x16_bf16, online softmax in fp32).  A workgroup owns 128
 // query rows of one prompt and one query head; each of its 4 wavefronts owns 32 rows.
-// K/V tiles of 64 keys are staged in LDS (K row-major with a 16-byte-chunk XOR swizzle,
-// V transposed to [dim][key]).  The wavefront computes the transposed score block
-// S^T = K Q^T, so a lane holds one query and 16 of its keys; the probabilities P^T then
-// already sit in the B-operand layout of O^T += V^T P^T once the 16 keys of each MFMA
-// step are taken in the order the score layout gives them (the contraction order is
-// free as long as both operands agree).  Row statistics are lane-local apart from one
-// exchange between the two 32-lane halves, which hold the same queries.
+// Two workgroups share a compute unit, so every SIMD runs two wavefronts and the
+// hardware overlaps one wavefront's softmax (vector ALU) with the other's MFMAs - a
+// single wavefront cannot issue vector instructions back to back.  The wavefront
+// computes the transposed score block S^T = K Q^T: a lane then holds one query and 16 of
+// its keys per 32-key block, and the probabilities P^T already sit in the B-operand
+// layout of O^T += V^T P^T once the 16 keys of each MFMA step are taken in the order the
+// score layout gives them (the contraction order is free as long as both operands agree).
+//
+// Keys move in 64-key tiles from HBM straight into LDS (global_load_lds_dwordx4) through
+// a 2-stage ring, the next tile loading while the current one is processed: K rows come
+// from the packed qkv rows, V from a transposed copy V^T [kv head * hd + dim][key] that
+// the QKV projection writes in its epilogue.  That copy gives each prompt a 64-aligned,
+// zero-padded column range and stores the keys of every 16-key group with index bits 2
+// and 3 swapped, so the 8 keys one lane feeds the PV MFMA are 16 contiguous bytes.  LDS
+// rows are 16-byte-chunk XOR-swizzled by the row.
+//
+// The running maximum is re-based lazily: O and the row sum are rescaled only when a row
+// maximum grows by more than 2^8 (probabilities stay below 256, well inside fp32 and bf16
+// range), which is exact up to rounding because numerator and denominator share the base.
 //
 // fp32 path: one thread per query row, exact expf, for the float32 model.
 #include "common.h"
@@ -17,136 +29,180 @@
 namespace surr {
 namespace {
 
-constexpr int kBQ = 128, kBKV = 64;
+constexpr int kBQ = 128, kBKV = 64, kStages = 2;
+constexpr float kLazy = 8.f;
+
+// DMA of 64-key tiles into ring stages.  Position p of a stage holds 16-byte chunk
+// (p % NCH) ^ (row % NCH) of K row p / NCH, then, for q = p - 64 NCH, chunk
+// (q % 8) ^ (d % 8) of V^T row d = q / 8.  Thread tid moves positions i * 256 + tid; its
+// byte offsets from the tile's K row k0 and V^T column k0 are fixed, so a tile costs a
+// uniform base and one load per position.  The tile that crosses the prompt's end clamps
+// K rows to the last one (keys past the prompt are masked; V^T columns stay inside the
+// prompt's padded range).
+template <int HD>
+struct AttnDma {
+    static constexpr int NCH = HD / 8, KCH = kBKV * NCH, HALF = KCH / 256;
+    uint32_t koff[HALF], voff[HALF];
+
+    __device__ __forceinline__ AttnDma(int64_t ld, int64_t ld_vt, int tid) {
+#pragma unroll
+        for (int i = 0; i < HALF; ++i) {
+            const int p = i * 256 + tid;
+            const int r = p / NCH, c = (p % NCH) ^ (r & (NCH - 1));
+            koff[i] = (uint32_t)((r * ld + c * 8) * 2);
+            const int d = p >> 3, cv = (p & 7) ^ (d & 7);
+            voff[i] = (uint32_t)((d * ld_vt + cv * 8) * 2);
+        }
+    }
+
+    __device__ __forceinline__ void issue(const uint16_t* kbase, int64_t ld, int L,
+                                          const uint16_t* vbase, int k0, uint32_t stage_lds,
+                                          int tid, int wave) const {
+        const uint16_t* kb = kbase + (int64_t)k0 * ld;
+        const uint16_t* vb = vbase + k0;
+        const uint32_t w = stage_lds + (uint32_t)wave * 64u * 16u;
+        if (k0 + kBKV <= L) {
+#pragma unroll
+            for (int i = 0; i < HALF; ++i) dma_load_16B_sbase(kb, koff[i], w + i * 256u * 16u);
+        } else {
+            const int rmax = L - 1 - k0;
+#pragma unroll
+            for (int i = 0; i < HALF; ++i) {
+                const int p = i * 256 + tid;
+                const int r = p / NCH, c = (p % NCH) ^ (r & (NCH - 1));
+                dma_load_16B_sbase(kb, (uint32_t)((min(r, rmax) * ld + c * 8) * 2),
+                                   w + i * 256u * 16u);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < HALF; ++i)
+            dma_load_16B_sbase(vb, voff[i], w + (HALF + i) * 256u * 16u);
+    }
+};
 
 template <int HD>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(const uint16_t* __restrict__ qkv,
-                                                        int64_t ld, uint16_t* __restrict__ out,
-                                                        int64_t ld_out,
-                                                        const int32_t* __restrict__ cu,
-                                                        const int2* __restrict__ work, int nqh,
-                                                        int nkvh, float scale_log2) {
-    constexpr int NCH = HD / 8;  // 16-byte chunks per K row
+__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
+    const uint16_t* __restrict__ qkv, int64_t ld, const uint16_t* __restrict__ vt, int64_t ld_vt,
+    const int32_t* __restrict__ vt_off, uint16_t* __restrict__ out, int64_t ld_out,
+    const int32_t* __restrict__ cu, const int2* __restrict__ work, int nqh, int nkvh,
+    float scale_log2) {
+    constexpr int NCH = HD / 8, KCH = kBKV * NCH, CHUNKS = 2 * KCH;
     constexpr int KS = HD / 16;  // MFMA steps over the head dim for S
     constexpr int DB = HD / 32;  // 32-dim blocks of O
-    constexpr int VTP = kBKV + 8;  // Vt row pitch in bf16 elements
-    __shared__ uint4 Ks[kBKV * NCH];
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[HD * VTP];
+    __shared__ uint4 lds[kStages * CHUNKS];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
     const int h = lane >> 5, l32 = lane & 31;
-    const int item = blockIdx.x / nqh, head = blockIdx.x - (blockIdx.x / nqh) * nqh;
+    const int item = blockIdx.x / nqh, head = blockIdx.x - item * nqh;
     const int2 wk = work[item];
     const int start = cu[wk.x], L = cu[wk.x + 1] - start;
     const int q0 = wk.y * kBQ;
     const int kvh = head * nkvh / nqh;
-    const int64_t k_col = (int64_t)(nqh + kvh) * HD, v_col = (int64_t)(nqh + nkvh + kvh) * HD;
-    const uint16_t* base = qkv + (int64_t)start * ld;
+    const uint16_t* kbase = qkv + (int64_t)start * ld + (int64_t)(nqh + kvh) * HD;
+    const uint16_t* vbase = vt + (int64_t)kvh * HD * ld_vt + vt_off[wk.x];
+    const uint32_t lds0 = lds_offset(lds);
 
-    const int qw0 = q0 + wave * 32;
+    const int kv_end = min(L, q0 + kBQ);
+    const int n_tiles = (kv_end + kBKV - 1) / kBKV;
+    const int qw0 = q0 + wave * 32;  // first query row of this wavefront
     const int my_q = qw0 + l32;
-    const bool wave_active = qw0 < L;
+    // tiles this wavefront needs: keys up to its last valid query row
+    const int wave_tiles = qw0 < L ? min(qw0 + 31, L - 1) / kBKV + 1 : 0;
 
     bf16x8 qf[KS];
     {
-        const uint16_t* qrow = base + (int64_t)min(my_q, L - 1) * ld + (int64_t)head * HD + 8 * h;
+        const uint16_t* qrow =
+            qkv + (int64_t)(start + min(my_q, L - 1)) * ld + (int64_t)head * HD + 8 * h;
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
-            qf[s] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qrow + 16 * s));
+        for (int st = 0; st < KS; ++st)
+            qf[st] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qrow + 16 * st));
     }
+    const AttnDma<HD> dma(ld, ld_vt, tid);
+    dma.issue(kbase, ld, L, vbase, 0, lds0, tid, wave);
 
     f32x16 o[DB];
 #pragma unroll
     for (int d = 0; d < DB; ++d) o[d] = f32x16{};
-    float m_run = -INFINITY, l_run = 0.f;
+    float m_ref = -INFINITY, l_sum = 0.f;
+    const int lim_q = min(my_q, L - 1);
 
-    const int kv_end = min(L, q0 + kBQ);
-    const int n_tiles = (kv_end + kBKV - 1) / kBKV;
+    wait_vmcnt<0>();
+    __syncthreads();
     for (int t = 0; t < n_tiles; ++t) {
-        const int k0 = t * kBKV;
-        __syncthreads();
-        for (int e = tid; e < kBKV * NCH; e += 256) {
-            const int r = e / NCH, c = e - (e / NCH) * NCH;
-            const int row = min(k0 + r, L - 1);
-            Ks[r * NCH + (c ^ (r & (NCH - 1)))] =
-                *reinterpret_cast<const uint4*>(base + (int64_t)row * ld + k_col + c * 8);
-        }
-        for (int e = tid; e < (kBKV / 2) * NCH; e += 256) {
-            const int p = e / NCH, c = e - (e / NCH) * NCH;
-            const int r0 = min(k0 + 2 * p, L - 1), r1 = min(k0 + 2 * p + 1, L - 1);
-            const uint4 a = *reinterpret_cast<const uint4*>(base + (int64_t)r0 * ld + v_col + c * 8);
-            const uint4 b = *reinterpret_cast<const uint4*>(base + (int64_t)r1 * ld + v_col + c * 8);
-            const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
-            uint32_t* dst = reinterpret_cast<uint32_t*>(Vt) + ((c * 8) * VTP + 2 * p) / 2;
+        if (t + 1 < n_tiles)  // its stage was released by the barrier that ended tile t - 1
+            dma.issue(kbase, ld, L, vbase, (t + 1) * kBKV,
+                      lds0 + (uint32_t)((t + 1) & 1) * CHUNKS * 16u, tid, wave);
+        if (t < wave_tiles) {
+            const uint4* Ks = lds + (t & 1) * CHUNKS;
+            const uint4* Vs = Ks + KCH;
+            // s[kb][4 j + i]: key 32 kb + 8 j + 4 h + i of the tile, query my_q
+            f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                dst[(2 * i) * (VTP / 2)] = (av[i] & 0xffffu) | (bv[i] << 16);
-                dst[(2 * i + 1) * (VTP / 2)] = (av[i] >> 16) | (bv[i] & 0xffff0000u);
-            }
-        }
-        __syncthreads();
-        if (!wave_active || k0 > qw0 + 31) continue;  // no key of this tile precedes a query
-
-        f32x16 s[2] = {f32x16{}, f32x16{}};
+            for (int kb = 0; kb < 2; ++kb) {
+                const int r = kb * 32 + l32;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            const int r = kb * 32 + l32;
-#pragma unroll
-            for (int st = 0; st < KS; ++st) {
-                const int chunk = 2 * st + h;
-                const bf16x8 a = __builtin_bit_cast(bf16x8, Ks[r * NCH + (chunk ^ (r & (NCH - 1)))]);
-                s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], s[kb], 0, 0, 0);
-            }
-        }
-        // s[kb][e]: key k0 + 32 kb + 8 (e / 4) + 4 h + e % 4, query my_q.
-        const bool need_mask = (k0 + kBKV - 1 > qw0) || (k0 + kBKV > L);
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                float v = s[kb][e] * scale_log2;
-                if (need_mask) {
-                    const int key = k0 + 32 * kb + 8 * (e >> 2) + 4 * h + (e & 3);
-                    if (key > my_q || key >= L) v = -INFINITY;
-                }
-                s[kb][e] = v;
-                mx = fmaxf(mx, v);
-            }
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m_run, mx);
-        const float corr = fast_exp2(m_run - m_new);
-        m_run = m_new;
-        l_run *= corr;
-#pragma unroll
-        for (int d = 0; d < DB; ++d) o[d] *= corr;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int s2 = 0; s2 < 2; ++s2) {
-                float pv[8];
-#pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    pv[i] = fast_exp2(s[kb][8 * s2 + i] - m_new);
-                    l_run += pv[i];
-                }
-                const uint4 pp = {pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
-                                  pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
-                const bf16x8 pb = __builtin_bit_cast(bf16x8, pp);
-#pragma unroll
-                for (int d = 0; d < DB; ++d) {
-                    const uint16_t* vr = Vt + (d * 32 + l32) * VTP + 32 * kb + 16 * s2 + 4 * h;
-                    const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-                    const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
-                    const uint4 vv = {lo.x, lo.y, hi.x, hi.y};
-                    o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv),
-                                                                   pb, o[d], 0, 0, 0);
+                for (int st = 0; st < KS; ++st) {
+                    const bf16x8 a =
+                        __builtin_bit_cast(bf16x8, Ks[r * NCH + ((2 * st + h) ^ (r & (NCH - 1)))]);
+                    s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], s[kb], 0, 0, 0);
                 }
             }
+            const int k0 = t * kBKV;
+            if (k0 + kBKV - 1 > qw0 || k0 + kBKV > L) {  // causal / length mask
+                const int lim = lim_q - (k0 + 4 * h);
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+                        s[kb][e] = 32 * kb + 8 * (e >> 2) + (e & 3) > lim ? -INFINITY : s[kb][e];
+            }
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kb][e]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            const float m_new = mx * scale_log2;
+            if (__any(m_new > m_ref + kLazy)) {
+                const bool up = m_new > m_ref + kLazy;
+                const float c = up ? fast_exp2(m_ref - m_new) : 1.f;
+                m_ref = up ? m_new : m_ref;
+                l_sum *= c;
+#pragma unroll
+                for (int d = 0; d < DB; ++d) o[d] *= c;
+            }
+            const float nm = -m_ref;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int s2 = 0; s2 < 2; ++s2) {
+                    float pv[8];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        pv[i] = fast_exp2(fmaf(s[kb][8 * s2 + i], scale_log2, nm));
+                        l_sum += pv[i];
+                    }
+                    const uint4 pp = {pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]),
+                                      pack_bf16x2(pv[4], pv[5]), pack_bf16x2(pv[6], pv[7])};
+                    const bf16x8 pb = __builtin_bit_cast(bf16x8, pp);
+#pragma unroll
+                    for (int d = 0; d < DB; ++d) {
+                        const int r = d * 32 + l32;
+                        const bf16x8 a = __builtin_bit_cast(
+                            bf16x8, Vs[r * 8 + ((4 * kb + 2 * s2 + h) ^ (r & 7))]);
+                        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[d], 0, 0, 0);
+                    }
+                }
+        }
+        if (t + 1 < n_tiles) {
+            wait_vmcnt<0>();  // this thread's part of tile t + 1
+            __syncthreads();  // all of tile t + 1 visible; stage t & 1 free
+        }
     }
-    l_run += __shfl_xor(l_run, 32, 64);
-    if (!wave_active || my_q >= L) return;
-    const float inv = 1.f / l_run;
+
+    if (wave_tiles == 0 || my_q >= L) return;
+    const float inv = 1.f / (l_sum + __shfl_xor(l_sum, 32, 64));
     uint16_t* orow = out + (int64_t)(start + my_q) * ld_out + (int64_t)head * HD + 4 * h;
 #pragma unroll
     for (int d = 0; d < DB; ++d)
@@ -221,18 +277,24 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 
 int attention_q_tile(Act t) { return t == Act::BF16 ? kBQ : kBQ32; }
 
-hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, void* out, int64_t ld_out,
-                            const int32_t* cu, const int2* work, int n_items, int n_q_heads,
-                            int n_kv_heads, int head_dim, hipStream_t s) {
+hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, const void* vt, int64_t ld_vt,
+                            const int32_t* vt_off, void* out, int64_t ld_out, const int32_t* cu,
+                            const int2* work, int n_items, int n_q_heads, int n_kv_heads,
+                            int head_dim, hipStream_t s) {
     if (n_items == 0) return hipSuccess;
     const unsigned grid = (unsigned)n_items * (unsigned)n_q_heads;
     if (t == Act::BF16) {
         const float sl2 = kLog2e / sqrtf((float)head_dim);
         const uint16_t* q = static_cast<const uint16_t*>(qkv);
+        const uint16_t* v = static_cast<const uint16_t*>(vt);
         uint16_t* o = static_cast<uint16_t*>(out);
+        // per-lane DMA offsets are 32-bit: V^T rows of one kv head and 64 K rows
+        if (!v || !vt_off || ld_vt % 8 || (int64_t)head_dim * ld_vt * 2 > UINT32_MAX ||
+            64 * ld_qkv * 2 > UINT32_MAX)
+            return hipErrorInvalidValue;
         switch (head_dim) {
-            case 64: attn_bf16_kernel<64><<<grid, 256, 0, s>>>(q, ld_qkv, o, ld_out, cu, work, n_q_heads, n_kv_heads, sl2); break;
-            case 128: attn_bf16_kernel<128><<<grid, 256, 0, s>>>(q, ld_qkv, o, ld_out, cu, work, n_q_heads, n_kv_heads, sl2); break;
+            case 64: attn_bf16_kernel<64><<<grid, 256, 0, s>>>(q, ld_qkv, v, ld_vt, vt_off, o, ld_out, cu, work, n_q_heads, n_kv_heads, sl2); break;
+            case 128: attn_bf16_kernel<128><<<grid, 256, 0, s>>>(q, ld_qkv, v, ld_vt, vt_off, o, ld_out, cu, work, n_q_heads, n_kv_heads, sl2); break;
             default: return hipErrorInvalidValue;
         }
     } else {

@@ -16,6 +16,8 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ 
                                                     int64_t T, const void* __restrict__ embed,
                                                     int d, int vocab, float* __restrict__ x,
                                                     int32_t* __restrict__ pos,
+                                                    const int32_t* __restrict__ vt_off,
+                                                    int32_t* __restrict__ vcol,
                                                     int32_t* __restrict__ err_flag) {
     const int lane = threadIdx.x & 63;
     const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -31,7 +33,10 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ 
         if (lane == 0) err_flag[0] = 1;
         tok = 0;
     }
-    if (lane == 0) pos[t] = j;
+    if (lane == 0) {
+        pos[t] = j;
+        if (vcol) vcol[t] = vt_off[lo] + vt_key_order(j);
+    }
     float4* xr = reinterpret_cast<float4*>(x + t * d);
     if constexpr (BF16) {
         const uint4* er = reinterpret_cast<const uint4*>(
@@ -47,6 +52,23 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ 
         const float4* er = reinterpret_cast<const float4*>(
             static_cast<const float*>(embed) + (int64_t)tok * d);
         for (int c = lane; c < d / 4; c += 64) xr[c] = er[c];
+    }
+}
+
+// ---------------------------------------------------------------- V^T padding
+// Prompt b owns columns [vt_off[b], vt_off[b + 1]) of the transposed V copy; stored
+// column c holds key vt_key_order(c), so the columns whose key is >= L_b are padding.
+// They start inside the last 16-key group at the earliest.
+__global__ __launch_bounds__(256) void vt_pad_zero_kernel(uint16_t* __restrict__ vt, int64_t ld_vt,
+                                                          int rows, const int32_t* __restrict__ cu,
+                                                          const int32_t* __restrict__ vt_off) {
+    const int b = blockIdx.x;
+    const int L = cu[b + 1] - cu[b], base = vt_off[b];
+    const int c0 = L & ~15, nc = vt_off[b + 1] - base - c0;
+    const int64_t n = (int64_t)rows * nc;
+    for (int64_t e = (int64_t)blockIdx.y * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.y * 256) {
+        const int r = (int)(e / nc), c = c0 + (int)(e - (int64_t)r * nc);
+        if (vt_key_order(c) >= L) vt[(int64_t)r * ld_vt + base + c] = 0;
     }
 }
 
@@ -270,13 +292,21 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 
 hipError_t launch_embed(Act wt, const int32_t* tokens, int64_t row_stride, const int32_t* cu,
                         int B, int64_t T, const void* embed, int d, int vocab, float* x,
-                        int32_t* pos, int32_t* err_flag, hipStream_t s) {
+                        int32_t* pos, const int32_t* vt_off, int32_t* vcol, int32_t* err_flag,
+                        hipStream_t s) {
     if (wt == Act::BF16)
         embed_kernel<true><<<blocks_for(T, 4), 256, 0, s>>>(tokens, row_stride, cu, B, T, embed,
-                                                            d, vocab, x, pos, err_flag);
+                                                            d, vocab, x, pos, vt_off, vcol, err_flag);
     else
         embed_kernel<false><<<blocks_for(T, 4), 256, 0, s>>>(tokens, row_stride, cu, B, T, embed,
-                                                             d, vocab, x, pos, err_flag);
+                                                             d, vocab, x, pos, vt_off, vcol, err_flag);
+    return hipGetLastError();
+}
+
+hipError_t launch_vt_pad_zero(uint16_t* vt, int64_t ld_vt, int rows, const int32_t* cu,
+                              const int32_t* vt_off, int B, hipStream_t s) {
+    if (B == 0 || rows == 0) return hipSuccess;
+    vt_pad_zero_kernel<<<dim3(B, 16), 256, 0, s>>>(vt, ld_vt, rows, cu, vt_off);
     return hipGetLastError();
 }
 

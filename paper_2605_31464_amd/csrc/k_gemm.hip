@@ -41,34 +41,7 @@ __device__ __forceinline__ int swz(int row) {
     else return (row >> 2) & 3;
 }
 
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N <= 63, "vmcnt");
-    // s_waitcnt simm16 on gfx9: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
 __device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); }
-
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-
-// Byte offset of a __shared__ object inside the workgroup's LDS allocation.
-__device__ __forceinline__ uint32_t lds_offset(const void* p) {
-    return (uint32_t)(uintptr_t)(lds_ptr_t)p;
-}
-
-// 16 bytes per lane from global memory straight into LDS at lds_addr + 16 * lane
-// (lds_addr is wave-uniform and goes through M0).  Written as inline assembly so the
-// compiler's wait-count model, which treats LDS DMA conservatively and would force a
-// full LDS-read drain before every MFMA group, does not see it: the kernel orders these
-// loads itself (explicit vmcnt waits and a barrier before any LDS read of the stage).
-__device__ __forceinline__ void dma_load_16B(const void* gptr, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-                 :
-                 : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
-                 : "memory", "m0");
-}
-
 
 // Tile order.  The hardware hands workgroup i to XCD i % 8, and each XCD has its own
 // L2.  With XCD remapping, XCD x receives the contiguous virtual range
@@ -309,6 +282,13 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
                         o2.y = pack_bf16x2(w[2], w[3]);
                         *reinterpret_cast<uint2*>(out + n) = o1;
                         *reinterpret_cast<uint2*>(out + n + half) = o2;
+                    } else if (rope.vt) {
+                        // V heads: transposed copy, column vcol[m] of rows n - cols
+                        const int64_t vc = rope.vcol[m];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            rope.vt[(int64_t)(n + e - rope.cols) * rope.ld_vt + vc] =
+                                (uint16_t)f32_to_bf16(acc[i][j][4 * q + e]);
                     } else {
 #pragma unroll
                         for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
@@ -360,13 +340,13 @@ hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void
 // Tile choice (measured on the 7B projection shapes): 256 x 256 x 32 tiles, eight
 // wavefronts of 128 x 64 (two per SIMD, so one hides the other's waits), a 3-stage ring
 // and XCD-grouped order; 128 x 128 tiles for the few-row GEMMs of the last-position
-// head and the pruned final layer.  The RoPE epilogue keeps four wavefronts of 128 x 128
-// so that each wavefront holds whole 128-wide heads.
+// head and the pruned final layer.  The RoPE epilogue uses wavefronts of 64 x 128 so
+// that each wavefront holds whole 128-wide heads.
 template <Epi EPI>
 hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                          int64_t ldc, int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
     if constexpr (EPI == Epi::StoreActRope) {  // RoPE needs a wave tile of whole heads
-        return run_bf16<256, 256, 32, 128, 128, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        return run_bf16<256, 256, 32, 64, 128, 3, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
     } else {
         if (M <= 128)
             return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);

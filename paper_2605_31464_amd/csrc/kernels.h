@@ -11,10 +11,18 @@ enum class Act { F32, BF16 };  // storage type of activations and matrices
 
 // ---- k_elementwise.hip
 // Gather embedding rows of the packed tokens into the fp32 residual x[T, d] and
-// record each token's position inside its prompt.  cu[B+1] are prompt offsets.
+// record each token's position inside its prompt.  cu[B+1] are prompt offsets.  With
+// vt_off (per-prompt first column of the transposed V copy), vcol[t] receives the token's
+// column there: vt_off[b] + vt_key_order(position).
 hipError_t launch_embed(Act wt, const int32_t* tokens, int64_t row_stride, const int32_t* cu,
                         int B, int64_t T, const void* embed, int d, int vocab, float* x,
-                        int32_t* pos, int32_t* err_flag, hipStream_t s);
+                        int32_t* pos, const int32_t* vt_off, int32_t* vcol, int32_t* err_flag,
+                        hipStream_t s);
+
+// Zero the padding columns of the transposed V copy (rows x [vt_off[b] + L_b,
+// vt_off[b + 1]) in stored order) so masked keys multiply finite values.
+hipError_t launch_vt_pad_zero(uint16_t* vt, int64_t ld_vt, int rows, const int32_t* cu,
+                              const int32_t* vt_off, int B, hipStream_t s);
 
 // y[r] = x[rows ? rows[r] : r] * rsqrt(mean(x^2) + eps) * g, stored as `out` type.
 hipError_t launch_rmsnorm(Act out, const float* x, int64_t ldx, const int32_t* rows,
@@ -49,12 +57,17 @@ enum class Epi { StoreAct, ResidAddF32, SwiGLU, StoreF32, StoreActRope };
 
 // Rotary embedding applied inside the GEMM epilogue (Epi::StoreActRope): columns
 // [0, cols) hold whole heads of head_dim; within each head, columns i and i + hd/2 of
-// row m rotate by the angle of position pos[m] (table cs[pos][i] = (cos, sin)).
+// row m rotate by the angle of position pos[m] (table cs[pos][i] = (cos, sin)).  With
+// vt set, columns [cols, N) (the V heads) go transposed to vt[n - cols][vcol[m]]
+// instead of C.
 struct RopeArgs {
     const int32_t* pos = nullptr;
     const float2* cs = nullptr;
     int cols = 0;
     int head_dim = 0;
+    uint16_t* vt = nullptr;
+    int64_t ld_vt = 0;
+    const int32_t* vcol = nullptr;
 };
 
 // C = A[M,K] * B[N,K]^T (both K-contiguous), fp32 accumulation, fused epilogue:
@@ -69,11 +82,13 @@ hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, 
 
 // ---- k_attention.hip
 // Causal GQA attention over the packed qkv rows.  work[i] = (prompt, q_tile) items;
-// grid = n_items * n_q_heads.  q_tile covers rows [q_tile * 128, +128) of the prompt
-// (64 rows for the fp32 kernel).
-hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, void* out, int64_t ld_out,
-                            const int32_t* cu, const int2* work, int n_items, int n_q_heads,
-                            int n_kv_heads, int head_dim, hipStream_t s);
+// grid = n_items * n_q_heads.  q_tile covers rows [q_tile * attention_q_tile, +tile) of
+// the prompt.  bf16 reads V from the transposed copy vt (see RopeArgs; ld_vt % 8 == 0,
+// vt_off[b] % 64 == 0); the fp32 kernel reads V from qkv and ignores vt.
+hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, const void* vt, int64_t ld_vt,
+                            const int32_t* vt_off, void* out, int64_t ld_out, const int32_t* cu,
+                            const int2* work, int n_items, int n_q_heads, int n_kv_heads,
+                            int head_dim, hipStream_t s);
 int attention_q_tile(Act t);
 
 }  // namespace surr

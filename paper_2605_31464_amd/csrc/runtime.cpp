@@ -47,8 +47,9 @@ struct LayerW {
 
 // Byte offsets of one call's workspace regions.
 struct WsLayout {
-    size_t cu, last, vid, work, work_last, pos, x, h, qkv, o, u, gu, o_last, x_last, h_last,
-        u_last, gu_last, y, logits, total;
+    size_t cu, last, vid, work, work_last, vt_off, pos, vcol, x, h, qkv, vt, o, u, gu, o_last,
+        x_last, h_last, u_last, gu_last, y, logits, total;
+    int64_t ld_vt;  // columns of the transposed V copy (bf16 models)
 };
 
 bool valid_config(const surrogate_config* c, std::string* why) {
@@ -136,10 +137,16 @@ WsLayout layout(const surrogate_model* m, int64_t B, int64_t T) {
     w.vid = take(4 * 16);
     w.work = take(8 * items);
     w.work_last = take(8 * B);
+    w.vt_off = take(4 * (B + 1));
     w.pos = take(4 * T);
+    // Transposed V copy: every prompt's keys start on a 64-column boundary, so its
+    // padded ranges need at most T + 63 B columns.
+    w.ld_vt = f32 ? 0 : (T + 63 * B + 63) / 64 * 64;
+    w.vcol = f32 ? 0 : take(4 * T);
     w.x = take(4 * T * c.d_model);
     w.h = take(e * T * c.d_model);
     w.qkv = take(e * T * m->d_qkv());
+    w.vt = f32 ? 0 : take(2 * (size_t)w.ld_vt * c.n_kv_heads * c.head_dim);
     w.o = take(e * T * m->d_q());
     w.u = take(e * T * c.d_ff);
     w.gu = f32 ? take(4 * T * 2 * c.d_ff) : 0;
@@ -331,7 +338,8 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
             return fail(SURR_E_SHAPE, "length of prompt " + std::to_string(b) + " outside [1, min(row_stride, max_pos)]");
         T += lengths_h[b];
     }
-    if (T > INT32_MAX) return fail(SURR_E_SHAPE, "total tokens exceed 2^31 - 1");
+    if (T + 64 * (int64_t)batch > INT32_MAX)
+        return fail(SURR_E_SHAPE, "total tokens plus 64 per prompt exceed 2^31 - 1");
     if (reinterpret_cast<uintptr_t>(workspace_d) % kAlign) return fail(SURR_E_INVALID_ARG, "workspace must be 256-byte aligned");
     const WsLayout w = layout(m, batch, T);
     if (workspace_bytes < w.total)
@@ -344,6 +352,8 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
         cu[b + 1] = cu[b] + lengths_h[b];
         last[b] = cu[b + 1] - 1;
     }
+    std::vector<int32_t> vt_off(batch + 1, 0);
+    for (int b = 0; b < batch; ++b) vt_off[b + 1] = vt_off[b] + (lengths_h[b] + 63) / 64 * 64;
     std::vector<int2> work, work_last(batch);
     for (int b = 0; b < batch; ++b) {
         for (int t = 0; t * qt < lengths_h[b]; ++t) work.push_back(make_int2(b, t));
@@ -355,7 +365,7 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
     std::stable_sort(work.begin(), work.end(),
                      [&](const int2& a, const int2& b) { return kv_len(a) > kv_len(b); });
 
-    const size_t meta_bytes = w.pos;  // cu .. work_last are contiguous from offset 0
+    const size_t meta_bytes = w.pos;  // cu .. vt_off are contiguous from offset 0
     {
         std::lock_guard<std::mutex> lock(m->mu);
         if (m->staged_pending) SURR_HIP(hipEventSynchronize(m->staged));
@@ -374,6 +384,7 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
         std::memcpy(P + w.vid, verdict_ids_h, 4 * (size_t)n_verdict);
         std::memcpy(P + w.work, work.data(), 8 * work.size());
         std::memcpy(P + w.work_last, work_last.data(), 8 * work_last.size());
+        std::memcpy(P + w.vt_off, vt_off.data(), 4 * vt_off.size());
         SURR_HIP(hipMemcpyAsync(workspace_d, P, meta_bytes, hipMemcpyHostToDevice, stream));
         SURR_HIP(hipEventRecord(m->staged, stream));
         m->staged_pending = true;
@@ -386,6 +397,10 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
     const int2* d_work = reinterpret_cast<const int2*>(W + w.work);
     const int2* d_work_last = reinterpret_cast<const int2*>(W + w.work_last);
     int32_t* d_pos = reinterpret_cast<int32_t*>(W + w.pos);
+    const bool bf16 = m->act == Act::BF16;
+    const int32_t* d_vt_off = bf16 ? reinterpret_cast<const int32_t*>(W + w.vt_off) : nullptr;
+    int32_t* d_vcol = bf16 ? reinterpret_cast<int32_t*>(W + w.vcol) : nullptr;
+    uint16_t* vt = bf16 ? reinterpret_cast<uint16_t*>(W + w.vt) : nullptr;
     float* x = reinterpret_cast<float*>(W + w.x);
     void* h = W + w.h;
     void* qkv = W + w.qkv;
@@ -443,7 +458,9 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
         return SURR_OK;
     };
 
-    SURR_PHASE_RUN(SURR_PHASE_EMBED, surr::launch_embed(a, tokens_d, row_stride, d_cu, batch, T, m->embed, d, c.vocab, x, d_pos, m->err_flag, stream));
+    SURR_PHASE_RUN(SURR_PHASE_EMBED, surr::launch_embed(a, tokens_d, row_stride, d_cu, batch, T, m->embed, d, c.vocab, x, d_pos, d_vt_off, d_vcol, m->err_flag, stream));
+    if (bf16)  // the projection epilogues never write these columns
+        SURR_PHASE_RUN(SURR_PHASE_EMBED, surr::launch_vt_pad_zero(vt, w.ld_vt, nkv * hd, d_cu, d_vt_off, batch, stream));
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerW& L = m->layers[l];
         const bool final_layer = l == c.n_layers - 1;
@@ -455,13 +472,16 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
             rope.cs = m->rope_cs;
             rope.cols = (nq + nkv) * hd;
             rope.head_dim = hd;
+            rope.vt = vt;
+            rope.ld_vt = w.ld_vt;
+            rope.vcol = d_vcol;
             SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream, rope));
         } else {
             SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreAct, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream));
             SURR_PHASE_RUN(SURR_PHASE_ROPE, surr::launch_rope(a, qkv, dqkv, T, d_pos, nq + nkv, hd, m->rope_cs, stream));
         }
         if (!final_layer) {
-            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, o, dq, d_cu, d_work, (int)work.size(), nq, nkv, hd, stream));
+            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, vt, w.ld_vt, d_vt_off, o, dq, d_cu, d_work, (int)work.size(), nq, nkv, hd, stream));
             SURR_PHASE_RUN(SURR_PHASE_GEMM_O, surr::launch_gemm(a, Epi::ResidAddF32, o, dq, L.w_o, dq, x, d, Ti, d, dq, stream));
             SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x, d, nullptr, T, L.mlp_norm, d, c.rms_eps, h, d, stream));
             const surrogate_status st = mlp(L, h, u, gu, x, Ti, SURR_PHASE_GEMM_GATE_UP, SURR_PHASE_GEMM_DOWN);
@@ -469,7 +489,7 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
         } else {
             // Only the last position of each prompt feeds the LM head: K/V above cover
             // every token; attention, O projection and MLP run for the last rows only.
-            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, o, dq, d_cu, d_work_last, batch, nq, nkv, hd, stream));
+            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, vt, w.ld_vt, d_vt_off, o, dq, d_cu, d_work_last, batch, nq, nkv, hd, stream));
             SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gather_rows(o, dq, d_last, batch, dq, (int)m->esz, o_last, dq, stream));
             SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gather_rows(x, d, d_last, batch, d, 4, x_last, d, stream));
             SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gemm(a, Epi::ResidAddF32, o_last, dq, L.w_o, dq, x_last, d, batch, d, dq, stream));
