@@ -16,7 +16,7 @@
 // the QKV projection writes in its epilogue.  That copy gives each prompt a 64-aligned,
 // zero-padded column range and stores the keys of every 16-key group with index bits 2
 // and 3 swapped, so the 8 keys one lane feeds the PV MFMA are 16 contiguous bytes.  LDS
-// rows are 16-byte-chunk XOR-swizzled by the row.
+// rows are 16-byte-chunk XOR-swizzled so fragment reads are free of bank conflicts.
 //
 // The running maximum is re-based lazily: O and the row sum are rescaled only when a row
 // maximum grows by more than 2^8 (probabilities stay below 256, well inside fp32 and bf16
@@ -32,9 +32,19 @@ namespace {
 constexpr int kBQ = 128, kBKV = 64, kStages = 2;
 constexpr float kLazy = 8.f;
 
+// 16-byte chunk order inside an LDS row of NCH chunks: XOR with a row function such that
+// 16 consecutive rows reading one logical chunk hit 16 distinct 16-byte bank groups of
+// the 256-byte bank line (a ds_read_b128 serves 16 lanes per pass).  256-byte rows
+// (NCH = 16) fill the line alone; 128-byte rows pair up, so the XOR uses row / 2.
+template <int NCH>
+__device__ __forceinline__ int lds_swz(int row) {
+    if constexpr (NCH == 16) return row & 15;
+    else return (row >> 1) & 7;
+}
+
 // DMA of 64-key tiles into ring stages.  Position p of a stage holds 16-byte chunk
-// (p % NCH) ^ (row % NCH) of K row p / NCH, then, for q = p - 64 NCH, chunk
-// (q % 8) ^ (d % 8) of V^T row d = q / 8.  Thread tid moves positions i * 256 + tid; its
+// (p % NCH) ^ lds_swz(row) of K row p / NCH, then, for q = p - 64 NCH, chunk
+// (q % 8) ^ lds_swz(d) of V^T row d = q / 8.  Thread tid moves positions i * 256 + tid; its
 // byte offsets from the tile's K row k0 and V^T column k0 are fixed, so a tile costs a
 // uniform base and one load per position.  The tile that crosses the prompt's end clamps
 // K rows to the last one (keys past the prompt are masked; V^T columns stay inside the
@@ -48,9 +58,9 @@ struct AttnDma {
 #pragma unroll
         for (int i = 0; i < HALF; ++i) {
             const int p = i * 256 + tid;
-            const int r = p / NCH, c = (p % NCH) ^ (r & (NCH - 1));
+            const int r = p / NCH, c = (p % NCH) ^ lds_swz<NCH>(r);
             koff[i] = (uint32_t)((r * ld + c * 8) * 2);
-            const int d = p >> 3, cv = (p & 7) ^ (d & 7);
+            const int d = p >> 3, cv = (p & 7) ^ lds_swz<8>(d);
             voff[i] = (uint32_t)((d * ld_vt + cv * 8) * 2);
         }
     }
@@ -69,7 +79,7 @@ struct AttnDma {
 #pragma unroll
             for (int i = 0; i < HALF; ++i) {
                 const int p = i * 256 + tid;
-                const int r = p / NCH, c = (p % NCH) ^ (r & (NCH - 1));
+                const int r = p / NCH, c = (p % NCH) ^ lds_swz<NCH>(r);
                 dma_load_16B_sbase(kb, (uint32_t)((min(r, rmax) * ld + c * 8) * 2),
                                    w + i * 256u * 16u);
             }
@@ -144,7 +154,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
 #pragma unroll
                 for (int st = 0; st < KS; ++st) {
                     const bf16x8 a =
-                        __builtin_bit_cast(bf16x8, Ks[r * NCH + ((2 * st + h) ^ (r & (NCH - 1)))]);
+                        __builtin_bit_cast(bf16x8, Ks[r * NCH + ((2 * st + h) ^ lds_swz<NCH>(r))]);
                     s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], s[kb], 0, 0, 0);
                 }
             }
@@ -190,7 +200,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
                     for (int d = 0; d < DB; ++d) {
                         const int r = d * 32 + l32;
                         const bf16x8 a = __builtin_bit_cast(
-                            bf16x8, Vs[r * 8 + ((4 * kb + 2 * s2 + h) ^ (r & 7))]);
+                            bf16x8, Vs[r * 8 + ((4 * kb + 2 * s2 + h) ^ lds_swz<8>(r))]);
                         o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[d], 0, 0, 0);
                     }
                 }
