@@ -94,7 +94,7 @@ template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
     const uint16_t* __restrict__ qkv, int64_t ld, const uint16_t* __restrict__ vt, int64_t ld_vt,
     const int32_t* __restrict__ vt_off, uint16_t* __restrict__ out, int64_t ld_out,
-    const int32_t* __restrict__ cu, const int2* __restrict__ work, int nqh, int nkvh,
+    const int32_t* __restrict__ cu, const int2* __restrict__ work, int n_items, int nqh, int nkvh,
     float scale_log2) {
     constexpr int NCH = HD / 8, KCH = kBKV * NCH, CHUNKS = 2 * KCH;
     constexpr int KS = HD / 16;  // MFMA steps over the head dim for S
@@ -104,7 +104,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
     const int h = lane >> 5, l32 = lane & 31;
-    const int item = blockIdx.x / nqh, head = blockIdx.x - item * nqh;
+    // Workgroup b runs on XCD b % 8.  XCD x takes work items x, x + 8, x + 16, ... (the
+    // host sorted them longest first) with all query heads of an item back to back, so
+    // the heads sharing a kv head read its K/V tiles through one XCD's L2.
+    const int xk = blockIdx.x >> 3;
+    const int item = 8 * (xk / nqh) + (blockIdx.x & 7), head = xk - (xk / nqh) * nqh;
+    if (item >= n_items) return;
     const int2 wk = work[item];
     const int start = cu[wk.x], L = cu[wk.x + 1] - start;
     const int q0 = wk.y * kBQ;
@@ -292,8 +297,8 @@ hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, const void* 
                             const int2* work, int n_items, int n_q_heads, int n_kv_heads,
                             int head_dim, hipStream_t s) {
     if (n_items == 0) return hipSuccess;
-    const unsigned grid = (unsigned)n_items * (unsigned)n_q_heads;
     if (t == Act::BF16) {
+        const unsigned grid = (unsigned)((n_items + 7) / 8 * 8) * (unsigned)n_q_heads;
         const float sl2 = kLog2e / sqrtf((float)head_dim);
         const uint16_t* q = static_cast<const uint16_t*>(qkv);
         const uint16_t* v = static_cast<const uint16_t*>(vt);
@@ -303,11 +308,12 @@ hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, const void* 
             64 * ld_qkv * 2 > UINT32_MAX)
             return hipErrorInvalidValue;
         switch (head_dim) {
-            case 64: attn_bf16_kernel<64><<<grid, 256, 0, s>>>(q, ld_qkv, v, ld_vt, vt_off, o, ld_out, cu, work, n_q_heads, n_kv_heads, sl2); break;
-            case 128: attn_bf16_kernel<128><<<grid, 256, 0, s>>>(q, ld_qkv, v, ld_vt, vt_off, o, ld_out, cu, work, n_q_heads, n_kv_heads, sl2); break;
+            case 64: attn_bf16_kernel<64><<<grid, 256, 0, s>>>(q, ld_qkv, v, ld_vt, vt_off, o, ld_out, cu, work, n_items, n_q_heads, n_kv_heads, sl2); break;
+            case 128: attn_bf16_kernel<128><<<grid, 256, 0, s>>>(q, ld_qkv, v, ld_vt, vt_off, o, ld_out, cu, work, n_items, n_q_heads, n_kv_heads, sl2); break;
             default: return hipErrorInvalidValue;
         }
     } else {
+        const unsigned grid = (unsigned)n_items * (unsigned)n_q_heads;
         const float sc = 1.f / sqrtf((float)head_dim);
         const float* q = static_cast<const float*>(qkv);
         float* o = static_cast<float*>(out);

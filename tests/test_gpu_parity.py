@@ -207,6 +207,19 @@ def test_hd128_gqa_shape_matches_oracle():
     assert_parity(out, oracle_for(shape, W, tok, L, vid), TOL["bf16"])
 
 
+def test_hd128_attention_tile_boundaries():
+    """Lengths on both sides of the 64-key tile and 128-query tile edges, one layer (the
+    attention output dominates the difference to the oracle), 15 prompts so the work list
+    is not a multiple of the 8 XCDs."""
+    shape = synth.CONFIGS["1p5b"].shape.replace(n_layers=1)
+    scorer, W = make_scorer(shape, gain_std=0.1, seed=3)
+    lengths = [63, 64, 65, 127, 128, 129, 191, 192, 193, 255, 256, 257, 383, 384, 385]
+    tok, L = padded(rng_prompts(shape.vocab, lengths, 17))
+    vid = [7, 11, shape.vocab - 1]
+    out = scorer.score(tok, L, vid)
+    assert_parity(out, oracle_for(shape, W, tok, L, vid), TOL["bf16"])
+
+
 def test_small_config_full_depth_sampled_prompts():
     w = synth.CONFIGS["small"]
     scorer, W = make_scorer(w.shape)
