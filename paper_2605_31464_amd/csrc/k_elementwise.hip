@@ -74,6 +74,8 @@ __global__ __launch_bounds__(256) void vt_pad_zero_kernel(uint16_t* __restrict__
 
 // ---------------------------------------------------------------- RMSNorm
 // One wavefront per row; fp32 sum of squares reduced in a fixed butterfly order.
+// Two passes over the row (the second mostly from L2); used for rows longer than the
+// single-pass kernel below holds in registers.
 template <bool OUT_BF16>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int64_t ldx,
                                                       const int32_t* __restrict__ rows,
@@ -106,6 +108,74 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
             reinterpret_cast<float4*>(static_cast<float*>(y) + r * ldy)[c] = make_float4(a, b, e, f);
         }
     }
+}
+
+// Single-pass form for rows of at most 256 * NC values: lane l keeps the float4 chunks
+// l, l + 64, ... of its row in registers, so x is read from HBM exactly once.  Same
+// arithmetic and reduction order as the two-pass kernel above.
+template <bool OUT_BF16, int NC>
+__global__ __launch_bounds__(256) void rmsnorm_reg_kernel(const float* __restrict__ x,
+                                                          int64_t ldx,
+                                                          const int32_t* __restrict__ rows,
+                                                          int64_t n_rows,
+                                                          const float* __restrict__ g, int d,
+                                                          float eps, void* __restrict__ y,
+                                                          int64_t ldy) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (r >= n_rows) return;
+    const int64_t src = rows ? (int64_t)rows[r] : r;
+    const float4* xr = reinterpret_cast<const float4*>(x + src * ldx);
+    const float4* g4 = reinterpret_cast<const float4*>(g);
+    const int n4 = d / 4;
+    float4 v[NC];
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+        const int c = lane + 64 * k;
+        v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (c < n4) v[k] = xr[c];
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int k = 0; k < NC; ++k)
+        if (lane + 64 * k < n4) ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
+    ss = wave_sum(ss);
+    const float sc = rsqrtf(ss / (float)d + eps);
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+        const int c = lane + 64 * k;
+        if (c >= n4) continue;
+        const float4 w = g4[c];
+        const float a = v[k].x * sc * w.x, b = v[k].y * sc * w.y, e = v[k].z * sc * w.z,
+                    f = v[k].w * sc * w.w;
+        if constexpr (OUT_BF16) {
+            uint2 o;
+            o.x = pack_bf16x2(a, b);
+            o.y = pack_bf16x2(e, f);
+            reinterpret_cast<uint2*>(static_cast<uint16_t*>(y) + r * ldy)[c] = o;
+        } else {
+            reinterpret_cast<float4*>(static_cast<float*>(y) + r * ldy)[c] = make_float4(a, b, e, f);
+        }
+    }
+}
+
+template <bool OUT_BF16>
+hipError_t rmsnorm_dispatch(const float* x, int64_t ldx, const int32_t* rows, int64_t n_rows,
+                            const float* g, int d, float eps, void* y, int64_t ldy,
+                            hipStream_t s) {
+    const unsigned grid = (unsigned)((n_rows + 3) / 4);
+    const int nc = (d / 4 + 63) / 64;
+#define SURR_RMS_REG(NC_)                                                                        \
+    rmsnorm_reg_kernel<OUT_BF16, NC_><<<grid, 256, 0, s>>>(x, ldx, rows, n_rows, g, d, eps, y, ldy)
+    if (nc <= 2) SURR_RMS_REG(2);
+    else if (nc <= 4) SURR_RMS_REG(4);
+    else if (nc <= 8) SURR_RMS_REG(8);
+    else if (nc <= 16) SURR_RMS_REG(16);
+    else if (nc <= 24) SURR_RMS_REG(24);
+    else
+        rmsnorm_kernel<OUT_BF16><<<grid, 256, 0, s>>>(x, ldx, rows, n_rows, g, d, eps, y, ldy);
+#undef SURR_RMS_REG
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------- RoPE
@@ -314,13 +384,8 @@ hipError_t launch_rmsnorm(Act out, const float* x, int64_t ldx, const int32_t* r
                           int64_t n_rows, const float* g, int d, float eps, void* y, int64_t ldy,
                           hipStream_t s) {
     if (n_rows == 0) return hipSuccess;
-    if (out == Act::BF16)
-        rmsnorm_kernel<true><<<blocks_for(n_rows, 4), 256, 0, s>>>(x, ldx, rows, n_rows, g, d,
-                                                                   eps, y, ldy);
-    else
-        rmsnorm_kernel<false><<<blocks_for(n_rows, 4), 256, 0, s>>>(x, ldx, rows, n_rows, g, d,
-                                                                    eps, y, ldy);
-    return hipGetLastError();
+    if (out == Act::BF16) return rmsnorm_dispatch<true>(x, ldx, rows, n_rows, g, d, eps, y, ldy, s);
+    return rmsnorm_dispatch<false>(x, ldx, rows, n_rows, g, d, eps, y, ldy, s);
 }
 
 hipError_t launch_rope(Act t, void* qkv, int64_t ld, int64_t T, const int32_t* pos, int n_heads,
