@@ -222,6 +222,112 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     // Lane owns row m = m0 + wm*WM + 32 i + (lane & 31) and, per 32-column fragment j,
     // columns nb + 8 q + 4 (lane >> 5) + {0..3} in acc[i][j][4 q + {0..3}].
     const int h = lane >> 5;
+
+    // ---- Staged epilogue.  Stored straight from the accumulators, one wavefront
+    // instruction would scatter 8- or 16-byte pieces over 32 rows, and with every CU
+    // reaching its epilogue at once those partial-line writes run far below HBM rate.
+    // Instead, once the LDS ring is idle, each fragment row i (32 rows of every row block)
+    // is written to LDS in output layout and the workgroup then stores it in 16-byte
+    // chunks, each wavefront instruction covering whole 512- or 1024-byte row segments
+    // (the residual of ResidAddF32 is read the same way).  Tiles holding transposed V
+    // columns keep the direct path below.
+    {
+        constexpr bool F32OUT = EPI == Epi::StoreF32 || EPI == Epi::ResidAddF32;
+        constexpr int ESZ = F32OUT ? 4 : 2;
+        constexpr int OCOLS = EPI == Epi::SwiGLU ? BN / 2 : BN;  // output columns per tile
+        constexpr int PROWS = (BM / WM) * 32;                    // rows per pass
+        constexpr int PITCH = OCOLS * ESZ + 16;                  // staged row, bytes
+        constexpr int RCH = OCOLS * ESZ / 16;                    // 16-byte chunks per row
+        static_assert(PROWS * PITCH <= NST * S::STAGE * 16, "staging fits the LDS ring");
+        const bool staged = EPI != Epi::StoreActRope || n0 + BN <= rope.cols;
+        if (staged) {
+            char* stg = reinterpret_cast<char*>(lds);
+            const int rl = wm * 32 + (lane & 31);  // staged row of this lane
+            const int ncol0 = EPI == Epi::SwiGLU ? n0 / 2 : n0;
+            const int nlim = EPI == Epi::SwiGLU ? N / 2 : N;
+            __syncthreads();  // every wavefront is done with the ring
+#pragma unroll
+            for (int i = 0; i < S::FM; ++i) {
+                char* srow = stg + rl * PITCH;
+                if constexpr (EPI == Epi::SwiGLU) {
+#pragma unroll
+                    for (int j = 0; j < S::FN; j += 2)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            float v[4];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                v[e] = silu(acc[i][j][4 * q + e]) * acc[i][j + 1][4 * q + e];
+                            const int col = (wn * WN + j * 32) / 2 + 8 * q + 4 * h;
+                            *reinterpret_cast<uint2*>(srow + col * 2) =
+                                make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+                        }
+                } else if constexpr (EPI == Epi::StoreActRope) {
+                    static_assert(WN % 128 == 0, "wave tile must hold whole 128-dim heads");
+                    const int m = min(m0 + wm * WM + i * 32 + (lane & 31), M - 1);
+                    const int hd = rope.head_dim, half = hd >> 1, fstep = hd / 64;
+                    const float2* cs = rope.cs + (int64_t)rope.pos[m] * half;
+#pragma unroll
+                    for (int j = 0; j < S::FN; ++j) {
+                        const int cb = wn * WN + j * 32;  // tile column of the fragment
+                        if (((n0 + cb) % hd) >= half) continue;  // written with its partner
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const int col = cb + 8 * q + 4 * h;
+                            float v[4], w[4];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                const float x1 = acc[i][j][4 * q + e];
+                                const float x2 = fstep == 1 ? acc[i][(j + 1) % S::FN][4 * q + e]
+                                                            : acc[i][(j + 2) % S::FN][4 * q + e];
+                                const float2 c = cs[(n0 + col + e) % hd];
+                                v[e] = x1 * c.x - x2 * c.y;
+                                w[e] = x2 * c.x + x1 * c.y;
+                            }
+                            *reinterpret_cast<uint2*>(srow + col * 2) =
+                                make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+                            *reinterpret_cast<uint2*>(srow + (col + half) * 2) =
+                                make_uint2(pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3]));
+                        }
+                    }
+                } else {
+#pragma unroll
+                    for (int j = 0; j < S::FN; ++j)
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const int col = wn * WN + j * 32 + 8 * q + 4 * h;
+                            if constexpr (F32OUT) {
+                                *reinterpret_cast<f32x4*>(srow + col * 4) =
+                                    f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1],
+                                          acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+                            } else {
+                                *reinterpret_cast<uint2*>(srow + col * 2) = make_uint2(
+                                    pack_bf16x2(acc[i][j][4 * q], acc[i][j][4 * q + 1]),
+                                    pack_bf16x2(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]));
+                            }
+                        }
+                }
+                __syncthreads();
+                for (int c = tid; c < PROWS * RCH; c += S::THREADS) {
+                    const int rr = c / RCH, cc = c - rr * RCH;
+                    const int m = m0 + (rr >> 5) * WM + i * 32 + (rr & 31);
+                    const int n = ncol0 + cc * (16 / ESZ);
+                    if (m >= M || n >= nlim) continue;
+                    const uint4 v = *reinterpret_cast<const uint4*>(stg + rr * PITCH + cc * 16);
+                    char* g = static_cast<char*>(C) + ((int64_t)m * ldc + n) * ESZ;
+                    if constexpr (EPI == Epi::ResidAddF32) {
+                        f32x4* p = reinterpret_cast<f32x4*>(g);
+                        *p = *p + __builtin_bit_cast(f32x4, v);
+                    } else {
+                        *reinterpret_cast<uint4*>(g) = v;
+                    }
+                }
+                __syncthreads();
+            }
+            return;
+        }
+    }
+
 #pragma unroll
     for (int i = 0; i < S::FM; ++i) {
         const int m = m0 + wm * WM + i * 32 + (lane & 31);
