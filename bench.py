@@ -45,6 +45,52 @@ def flops_per_prompt(s, L: np.ndarray) -> np.ndarray:
             + 4 * s.n_q_heads * s.head_dim * L + 2 * d * s.vocab)
 
 
+PEAK_HBM = 8.0e12  # bytes/s, MI355X HBM3E
+
+
+def phase_rates(s, L: np.ndarray, phases: dict, steps: int) -> dict:
+    """Achieved rate of each phase against its roofline, from the phase times measured
+    with HIP events on the launch stream: MFMA phases in TFLOP/s of algorithmic work,
+    memory-bound phases in GB/s of algorithmic bytes (each tensor read or written once).
+    Per step at the batch's lengths: QKV over all T tokens in every layer (the final
+    layer needs every token's K and V); O, gate/up and down over T in the non-final
+    layers; attention on the causal triangle in the non-final layers plus the last row of
+    each prompt in the final one; RMSNorm = 2 n_layers - 1 full-batch norms (fp32 row in,
+    bf16 row out) plus two on the last rows; the head reads W_head once and writes B rows
+    of logits; embedding gathers bf16 rows into the fp32 residual."""
+    d, dq, dkv, ff, V = s.d_model, s.d_q, s.d_kv, s.d_ff, s.vocab
+    nl, T, B_ = s.n_layers, float(L.sum()), float(len(L))
+    esz = 2 if s.dtype == "bf16" else 4
+    Lf = L.astype(np.float64)
+    work = {
+        "gemm_qkv": ("mfma", 2.0 * d * (dq + 2 * dkv) * T * nl),
+        "gemm_o": ("mfma", 2.0 * dq * d * T * (nl - 1)),
+        "gemm_gate_up": ("mfma", 2.0 * d * 2 * ff * T * (nl - 1)),
+        "gemm_down": ("mfma", 2.0 * ff * d * T * (nl - 1)),
+        "attention": ("mfma", (nl - 1) * float((2 * s.n_q_heads * s.head_dim * Lf * (Lf + 1)).sum())
+                      + float((4 * s.n_q_heads * s.head_dim * Lf).sum())),
+        "embed": ("hbm", T * (esz * d + 4 * d + 12)),
+        "rmsnorm": ("hbm", ((2 * nl - 1) * T + 2 * B_) * (4 * d + esz * d)),
+        "lm_head": ("hbm", esz * V * d + esz * B_ * d + 4 * B_ * V),
+        "lse_verdict": ("hbm", 4 * B_ * V),
+    }
+    out = {}
+    for ph, (bound, amount) in work.items():
+        ms, n = phases.get(ph, (0.0, 0))
+        if not n or ms <= 0:
+            continue
+        t = ms / steps / 1e3
+        if bound == "mfma":
+            ach = amount / t
+            out[ph] = {"bound": "mfma", "achieved": ach / 1e12, "unit": "TFLOP/s",
+                       "frac": ach / PEAK_BF16, "ms_per_step": ms / steps}
+        else:
+            ach = amount / t
+            out[ph] = {"bound": "hbm", "achieved": ach / 1e9, "unit": "GB/s",
+                       "frac": ach / PEAK_HBM, "ms_per_step": ms / steps}
+    return out
+
+
 def cpu_baseline(shape, W, tok, L, vid) -> dict:
     """Time the float64 oracle on a bounded sample of the same workload and scale it to
     pairs/s: layers 0-7 of the model over the first 1024 tokens of the shortest prompt,
@@ -226,6 +272,7 @@ def main() -> int:
                                "frac": ach / PEAK_BF16,
                                "traffic": measured_traffic(args.config),
                                "avg_launch_ms": avg_s * 1e3, "launches": n}
+        out["phase_rates"] = phase_rates(s, L.astype(np.int64), phases, args.steps)
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(s, W, tok_np, L, vid)
