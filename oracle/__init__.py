@@ -15,10 +15,14 @@ definition:
 * ``select``      - selective use (Section 2.1, Selective Use) with the threshold
   convention s >= tau of Section 3.6, and the budgeted measurement of the lowest-
   confidence k candidates (Section 3.1 measures a top-c% subset).
+* ``forecast``    - the paper's eight-bin speedup head: expected speedup
+  S_hat = sum_b p_b m_b (Section 3.1, Table 3), discovery score Pr[g >= x]
+  (Section 3.6) and the top-k candidates by S_hat (Sections 3.1 and 3.5).
 
-Parity status: every function is pinned by ``tests/test_oracle_pins.py`` (closed
+Parity status: every function is pinned by ``tests/test_oracle_pins.py`` and
+``tests/test_oracle_forecast_pins.py`` (closed
 forms, invariants, a hand-computed one-layer case, independent library routines,
 brute force).  The absolute bf16 error at full depth has no closed form; it is
 bounded only by comparison with this oracle at the stated tolerances.
 """
-from . import select, transformer  # noqa: F401
+from . import forecast, select, transformer  # noqa: F401

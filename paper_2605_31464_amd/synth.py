@@ -206,3 +206,17 @@ def make_prompts(w: Workload, seed: int = 1, pad: int = 0, lengths=None):
 def verdict_ids(w: Workload) -> np.ndarray:
     V = w.shape.vocab
     return np.arange(V - w.n_verdict, V, dtype=np.int32)
+
+
+def bin_forecasts(n: int, n_bins: int = 8, seed: int = 2) -> np.ndarray:
+    """Forecast distributions over speedup bins, float32 [n, n_bins].
+
+    Row i is a Dirichlet draw with all concentrations equal to alpha_i, where
+    log10(alpha_i) is uniform on [-1, 1]: small alpha gives peaked forecasts, large
+    alpha nearly flat ones.  ``default_rng(seed)`` draws the alphas, then the rows.
+    """
+    rng = np.random.default_rng(seed)
+    alpha = 10.0 ** rng.uniform(-1.0, 1.0, size=n)
+    g = rng.gamma(alpha[:, None], 1.0, size=(n, n_bins))
+    g = np.maximum(g, 1e-30)
+    return (g / g.sum(axis=1, keepdims=True)).astype(np.float32)
