@@ -45,9 +45,6 @@ def flops_per_prompt(s, L: np.ndarray) -> np.ndarray:
             + 4 * s.n_q_heads * s.head_dim * L + 2 * d * s.vocab)
 
 
-PEAK_HBM = 8.0e12  # bytes/s, MI355X HBM3E
-
-
 def phase_rates(s, L: np.ndarray, phases: dict, steps: int) -> dict:
     """Achieved rate of each phase against its roofline, from the phase times measured
     with HIP events on the launch stream: MFMA phases in TFLOP/s of algorithmic work,
@@ -89,6 +86,43 @@ def phase_rates(s, L: np.ndarray, phases: dict, steps: int) -> dict:
             out[ph] = {"bound": "hbm", "achieved": ach / 1e9, "unit": "GB/s",
                        "frac": ach / PEAK_HBM, "ms_per_step": ms / steps}
     return out
+
+
+def forecast_head_rates(B, torch, dev, n: int = 65536, reps: int = 200) -> dict:
+    """Latency and achieved HBM rate of the eight-bin forecast head (expected speedup and
+    three discovery cutoffs) and of top-quarter selection by expected speedup, on n
+    seeded forecasts resident in HBM.  Algorithmic bytes per head call: the forecasts
+    (4 n_bins B per row) read once, 4 (1 + n_cutoffs) B per row written."""
+    from paper_2605_31464_amd import synth
+    nb, cut = 8, (1.25, 1.5, 2.0)
+    edges = [2.0 ** e for e in (-2.0, -1.0, -0.5, 0.0, 0.5, 1.0, 2.0)]
+    m = [0.17, 0.35, 0.59, 0.84, 1.19, 1.68, 2.83, 5.6]  # open-bin means: synthetic values
+    probs = torch.from_numpy(synth.bin_forecasts(n, nb, seed=3)).to(dev)
+    sp = torch.empty(n, device=dev)
+    disc = torch.empty(n, len(cut), device=dev)
+    d_idx = torch.empty(n, dtype=torch.int32, device=dev)
+    a_idx = torch.empty(n, dtype=torch.int32, device=dev)
+    counts = torch.empty(2, dtype=torch.int32, device=dev)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3  # microseconds
+
+    us_head = timed(lambda: B.surrogate_forecast_head(probs, m, edges, cut, sp, disc))
+    us_sel = timed(lambda: B.surrogate_select(sp, B.SURR_SELECT_TOP_SCORE, 0.0, n // 4, d_idx,
+                                              a_idx, counts))
+    nbytes = n * (4 * nb + 4 * (1 + len(cut)))
+    return {"n": n, "n_bins": nb, "n_cutoffs": len(cut), "us_per_call": us_head,
+            "bytes": nbytes, "achieved_GBps": nbytes / (us_head * 1e-6) / 1e9,
+            "frac_of_hbm": nbytes / (us_head * 1e-6) / PEAK_HBM, "bound": "launch latency",
+            "select_top_quarter_us": us_sel}
 
 
 def cpu_baseline(shape, W, tok, L, vid) -> dict:
@@ -153,6 +187,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the per-phase HIP-event timing (the roofline block)")
+    ap.add_argument("--no-forecast-head", action="store_true",
+                    help="skip timing the eight-bin forecast head and top-score selection")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one device-to-device copy of this size first (reference "
                          "dispatch for scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
@@ -273,6 +309,8 @@ def main() -> int:
                                "traffic": measured_traffic(args.config),
                                "avg_launch_ms": avg_s * 1e3, "launches": n}
         out["phase_rates"] = phase_rates(s, L.astype(np.int64), phases, args.steps)
+    if not args.no_forecast_head:
+        out["forecast_head"] = forecast_head_rates(B, torch, dev)
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(s, W, tok_np, L, vid)

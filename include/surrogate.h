@@ -9,7 +9,10 @@
  * distribution p_i, a predicted verdict (argmax) and a confidence q_i = max_b p_{i,b}
  * (Section 2.1).  Selective use (Section 2.1, Selective Use; budgeted measurement in
  * Section 3.1) then splits a batch into forecasts to accept and candidates to defer
- * to GPU measurement.
+ * to GPU measurement.  With the paper's eight speedup bins (Table 3) the forecast head
+ * also gives each candidate an expected speedup, by which a search measures only the
+ * best-ranked candidates (Sections 3.1 and 3.5), and discovery scores Pr[g >= x]
+ * (Section 3.6).
  *
  * Conventions shared by every call:
  *  - Every call returns a surrogate_status; 0 is success, negative values are errors.
@@ -48,7 +51,11 @@ typedef enum {
 
 typedef enum { SURR_F32 = 0, SURR_BF16 = 1 } surrogate_dtype;
 
-typedef enum { SURR_SELECT_THRESHOLD = 0, SURR_SELECT_BUDGET = 1 } surrogate_select_mode;
+typedef enum {
+    SURR_SELECT_THRESHOLD = 0,
+    SURR_SELECT_BUDGET = 1,
+    SURR_SELECT_TOP_SCORE = 2
+} surrogate_select_mode;
 
 typedef struct surrogate_model surrogate_model; /* opaque: device weights + RoPE table */
 
@@ -123,12 +130,19 @@ surrogate_status surrogate_score_pairs(surrogate_model *m, const int32_t *tokens
                                        float *confidence_d, int32_t *verdict_d,
                                        hipStream_t stream);
 
-/* Selective deferral on a device confidence vector confidence_d[n], 1 <= n <= 65536.
+/* Selective deferral on a device score vector confidence_d[n], 1 <= n <= 65536.  The
+ * first list ("defer") is always the set sent to measurement on the device.
  *  SURR_SELECT_THRESHOLD: accept i iff confidence[i] >= threshold in float32 (the
  *    convention s >= tau of Section 3.6); NaN is never accepted.  budget_k is ignored.
+ *    With discovery scores (surrogate_forecast_head) as input, the accepted list is the
+ *    set predicted to be discovery moments.
  *  SURR_SELECT_BUDGET: defer the min(budget_k, n) candidates of lowest confidence
  *    (Section 3.1 measures a budgeted subset); order is confidence ascending with NaN
  *    first, ties by ascending index, -0.0 == +0.0.  budget_k < 0 is an error.
+ *  SURR_SELECT_TOP_SCORE: the vector holds expected speedups S_hat; defer (measure) the
+ *    min(budget_k, n) candidates of highest score, the top-c% of Section 3.1 and the
+ *    best quarter a search measures in Section 3.5; order is score descending with NaN
+ *    last, ties by ascending index, -0.0 == +0.0.  budget_k < 0 is an error.
  * Outputs (device): defer_idx_d[n] and accept_idx_d[n] receive the ascending index
  * lists (entries past each count are left untouched); counts_d[2] = {n_defer,
  * n_accept}, which sum to n.  Bit-exact and deterministic. */
@@ -136,6 +150,30 @@ surrogate_status surrogate_select(const float *confidence_d, int32_t n,
                                   surrogate_select_mode mode, float threshold, int32_t budget_k,
                                   int32_t *defer_idx_d, int32_t *accept_idx_d, int32_t *counts_d,
                                   hipStream_t stream);
+
+/* The speedup-bin forecast head on forecasts probs_d[n, n_bins] (device, row-major,
+ * e.g. the probs_d of surrogate_score_pairs with one verdict token per bin).
+ *  bin_values_h  host [n_bins]: representative speedup m_b of each bin (Table 3: the
+ *                interior values are geometric bin centres; the open first and last bins
+ *                take empirical means, which the caller supplies).
+ *  bin_edges_h   host [n_bins - 1], positive, strictly increasing: bin b covers
+ *                (edge[b-1], edge[b]], the first bin everything up to edge[0], the last
+ *                everything above edge[n_bins - 2].  Read only if n_cutoffs > 0.
+ *  cutoffs_h     host [n_cutoffs], each in [edge[0], edge[n_bins - 2]].
+ * Outputs (device, either may be NULL):
+ *  expected_speedup_d  float [n]: S_hat_i = sum_b p_{i,b} m_b (Section 3.1).
+ *  discovery_d         float [n, n_cutoffs]: s_i = Pr[g >= x_c] under p_i (Section 3.6),
+ *                      with each interior bin's mass spread log-uniformly over the bin;
+ *                      a cutoff on an edge sums whole bins.
+ * 1 <= n_bins <= 16, 0 <= n_cutoffs <= 8 (n_bins >= 2 when n_cutoffs > 0), n >= 0.
+ * Computed in float32 with the per-bin weights formed in float64 on the host.
+ * Errors (synchronous, nothing enqueued): SURR_E_INVALID_ARG for nulls, counts out of
+ * range, non-finite values, unordered edges or a cutoff outside the edges; SURR_E_HIP. */
+surrogate_status surrogate_forecast_head(const float *probs_d, int64_t n, int32_t n_bins,
+                                         const double *bin_values_h, const double *bin_edges_h,
+                                         const double *cutoffs_h, int32_t n_cutoffs,
+                                         float *expected_speedup_d, float *discovery_d,
+                                         hipStream_t stream);
 
 /* Synchronize `stream` and report (then clear) the sticky device error of the model:
  * SURR_E_TOKEN_RANGE if an out-of-range token id was seen since the last check. */

@@ -22,13 +22,13 @@ SURR_E_HIP = -5
 SURR_E_WEIGHTS = -6
 SURR_E_WORKSPACE = -7
 SURR_F32, SURR_BF16 = 0, 1
-SURR_SELECT_THRESHOLD, SURR_SELECT_BUDGET = 0, 1
+SURR_SELECT_THRESHOLD, SURR_SELECT_BUDGET, SURR_SELECT_TOP_SCORE = 0, 1, 2
 
 EXPORTS = ("surrogate_tensor_count", "surrogate_tensor_shape", "surrogate_load_weights",
            "surrogate_get_config", "surrogate_workspace_size", "surrogate_score_pairs",
            "surrogate_select", "surrogate_device_status", "surrogate_free",
            "surrogate_status_string", "surrogate_last_error", "surrogate_profile_enable",
-           "surrogate_profile_collect")
+           "surrogate_profile_collect", "surrogate_forecast_head")
 PHASES = ("embed", "rmsnorm", "gemm_qkv", "rope", "attention", "gemm_o", "gemm_gate_up",
           "gemm_down", "last_rows", "lm_head", "lse_verdict")
 
@@ -75,6 +75,7 @@ def lib() -> ctypes.CDLL:
         "surrogate_last_error": (ctypes.c_char_p, []),
         "surrogate_profile_enable": (I32, [P, I32]),
         "surrogate_profile_collect": (I32, [P, P, P]),
+        "surrogate_forecast_head": (I32, [P, I64, I32, P, P, P, I32, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -207,6 +208,32 @@ def surrogate_select(confidence, mode: int, threshold: float = 0.0, budget_k: in
                                   ctypes.c_void_p(counts.data_ptr()),
                                   ctypes.c_void_p(_stream(stream))), "surrogate_select")
     return defer_idx, accept_idx, counts
+
+
+def surrogate_forecast_head(probs, bin_values, bin_edges=None, cutoffs=(), expected_speedup=None,
+                            discovery=None, want_speedup=True, stream=None):
+    """probs: float32 device [n, n_bins]; bin_values, bin_edges, cutoffs: host sequences.
+    Returns (expected_speedup [n] or None, discovery [n, n_cutoffs] or None)."""
+    import torch
+    if probs.dtype != torch.float32 or probs.dim() != 2 or not probs.is_contiguous():
+        raise ValueError("probs must be a contiguous float32 [n, n_bins] device tensor")
+    n, nb = int(probs.shape[0]), int(probs.shape[1])
+    m = np.ascontiguousarray(np.asarray(bin_values, np.float64))
+    if m.shape != (nb,):
+        raise ValueError("bin_values must have n_bins entries")
+    cut = np.ascontiguousarray(np.asarray(cutoffs, np.float64).reshape(-1))
+    nc = int(cut.size)
+    e = None if bin_edges is None else np.ascontiguousarray(np.asarray(bin_edges, np.float64))
+    if want_speedup and expected_speedup is None:
+        expected_speedup = torch.empty(n, dtype=torch.float32, device=probs.device)
+    if nc and discovery is None:
+        discovery = torch.empty(n, nc, dtype=torch.float32, device=probs.device)
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
+    host = lambda a: ctypes.c_void_p(a.ctypes.data if a is not None and a.size else 0)
+    _check(lib().surrogate_forecast_head(
+        ptr(probs), n, nb, host(m), host(e), host(cut), nc, ptr(expected_speedup),
+        ptr(discovery if nc else None), ctypes.c_void_p(_stream(stream))), "surrogate_forecast_head")
+    return expected_speedup, (discovery if nc else None)
 
 
 def surrogate_device_status(model: Model, stream=None) -> int:

@@ -291,7 +291,9 @@ __global__ __launch_bounds__(256) void lse_verdict_kernel(const float* __restric
 
 // ---------------------------------------------------------------- selection
 // flags[i] = 1 if candidate i is deferred.  Threshold: !(q_i >= tau).  Budget: the rank
-// of i in the order (NaN first, confidence ascending, index ascending) is below k.
+// of i in the order (NaN first, confidence ascending, index ascending) is below k.  Top
+// score: the rank of i in the order (score descending, NaN last, index ascending) is
+// below k; that is the budget order on the key -score with NaN mapped to +inf.
 __global__ __launch_bounds__(256) void select_flags_kernel(const float* __restrict__ q, int n,
                                                            int mode, float tau, int k,
                                                            int32_t* __restrict__ flags) {
@@ -303,13 +305,14 @@ __global__ __launch_bounds__(256) void select_flags_kernel(const float* __restri
         if (i < n) flags[i] = !(qi >= tau);
         return;
     }
-    const float ki = __builtin_isnan(qi) ? -INFINITY : qi;
+    const bool top = mode == 2;
+    const float ki = __builtin_isnan(qi) ? (top ? INFINITY : -INFINITY) : (top ? -qi : qi);
     int rank = 0;
     for (int j0 = 0; j0 < n; j0 += 256) {
         __syncthreads();
         const int j = j0 + tid;
         const float qj = j < n ? q[j] : 0.f;
-        keys[tid] = __builtin_isnan(qj) ? -INFINITY : qj;
+        keys[tid] = __builtin_isnan(qj) ? (top ? INFINITY : -INFINITY) : (top ? -qj : qj);
         __syncthreads();
         const int lim = min(256, n - j0);
         for (int jj = 0; jj < lim; ++jj) {

@@ -47,10 +47,25 @@ hipError_t launch_lse_verdict(const float* logits, int64_t ld, int B, int V, con
                               int nv, float* lp, float* probs, float* conf, int32_t* verdict,
                               hipStream_t s);
 
-// Selection: flags then ordered compaction.
+// Selection: flags then ordered compaction.  mode 0: defer !(q >= tau); mode 1: defer the
+// k lowest (NaN first); mode 2: defer the k highest (NaN last); ties by ascending index.
 hipError_t launch_select(const float* conf, int n, int mode, float tau, int k, int32_t* flags,
                          int32_t* defer_idx, int32_t* accept_idx, int32_t* counts,
                          hipStream_t s);
+
+// ---- k_forecast.hip
+constexpr int kMaxBins = 16, kMaxCutoffs = 8;
+
+// Per-bin weights of the forecast head: w[b][0] = representative speedup m_b,
+// w[b][1 + c] = share of bin b's mass at or above cutoff c.
+struct BinWeights {
+    float w[kMaxBins][1 + kMaxCutoffs];
+};
+
+// speedup[i] = sum_b probs[i, b] w[b][0] and disc[i, c] = sum_b probs[i, b] w[b][1 + c]
+// (either output may be null), probs row-major [n, n_bins].
+hipError_t launch_forecast_head(const float* probs, int64_t n, int n_bins, const BinWeights& w,
+                                int n_cutoffs, float* speedup, float* disc, hipStream_t s);
 
 // ---- k_gemm.hip
 enum class Epi { StoreAct, ResidAddF32, SwiGLU, StoreF32, StoreActRope };

@@ -511,12 +511,65 @@ surrogate_status surrogate_select(const float* confidence_d, int32_t n, surrogat
     if (!confidence_d || !defer_idx_d || !accept_idx_d || !counts_d)
         return fail(SURR_E_INVALID_ARG, "null argument");
     if (n < 1 || n > 65536) return fail(SURR_E_INVALID_ARG, "n must be in [1, 65536]");
-    if (mode != SURR_SELECT_THRESHOLD && mode != SURR_SELECT_BUDGET)
+    if (mode != SURR_SELECT_THRESHOLD && mode != SURR_SELECT_BUDGET && mode != SURR_SELECT_TOP_SCORE)
         return fail(SURR_E_INVALID_ARG, "unknown select mode");
-    if (mode == SURR_SELECT_BUDGET && budget_k < 0) return fail(SURR_E_INVALID_ARG, "budget_k must be >= 0");
-    const int k = mode == SURR_SELECT_BUDGET ? std::min(budget_k, n) : 0;
-    SURR_HIP(surr::launch_select(confidence_d, n, mode == SURR_SELECT_BUDGET ? 1 : 0, threshold, k,
-                                 defer_idx_d, defer_idx_d, accept_idx_d, counts_d, stream));
+    const bool ranked = mode != SURR_SELECT_THRESHOLD;
+    if (ranked && budget_k < 0) return fail(SURR_E_INVALID_ARG, "budget_k must be >= 0");
+    const int k = ranked ? std::min(budget_k, n) : 0;
+    const int kmode = mode == SURR_SELECT_THRESHOLD ? 0 : mode == SURR_SELECT_BUDGET ? 1 : 2;
+    SURR_HIP(surr::launch_select(confidence_d, n, kmode, threshold, k, defer_idx_d, defer_idx_d,
+                                 accept_idx_d, counts_d, stream));
+    return SURR_OK;
+}
+
+surrogate_status surrogate_forecast_head(const float* probs_d, int64_t n, int32_t n_bins,
+                                         const double* bin_values_h, const double* bin_edges_h,
+                                         const double* cutoffs_h, int32_t n_cutoffs,
+                                         float* expected_speedup_d, float* discovery_d,
+                                         hipStream_t stream) {
+    using surr::kMaxBins;
+    using surr::kMaxCutoffs;
+    if (n < 0) return fail(SURR_E_INVALID_ARG, "n must be >= 0");
+    if (n_bins < 1 || n_bins > kMaxBins) return fail(SURR_E_INVALID_ARG, "n_bins must be in [1, 16]");
+    if (n_cutoffs < 0 || n_cutoffs > kMaxCutoffs) return fail(SURR_E_INVALID_ARG, "n_cutoffs must be in [0, 8]");
+    if (!bin_values_h) return fail(SURR_E_INVALID_ARG, "null bin values");
+    if (n > 0 && !probs_d && (expected_speedup_d || discovery_d)) return fail(SURR_E_INVALID_ARG, "null probs");
+    if (n_cutoffs > 0 && (n_bins < 2 || !bin_edges_h || !cutoffs_h))
+        return fail(SURR_E_INVALID_ARG, "discovery cutoffs need n_bins >= 2, edges and cutoffs");
+    if (n > INT64_MAX / kMaxBins) return fail(SURR_E_INVALID_ARG, "n too large");
+    surr::BinWeights w{};
+    for (int b = 0; b < n_bins; ++b) {
+        if (!std::isfinite(bin_values_h[b])) return fail(SURR_E_INVALID_ARG, "non-finite bin value");
+        w.w[b][0] = (float)bin_values_h[b];
+    }
+    if (n_cutoffs > 0) {
+        const int ne = n_bins - 1;
+        for (int j = 0; j < ne; ++j) {
+            if (!std::isfinite(bin_edges_h[j]) || !(bin_edges_h[j] > 0.0) ||
+                (j > 0 && !(bin_edges_h[j] > bin_edges_h[j - 1])))
+                return fail(SURR_E_INVALID_ARG, "bin edges must be finite, positive, strictly increasing");
+        }
+        for (int c = 0; c < n_cutoffs; ++c) {
+            const double x = cutoffs_h[c];
+            if (!(x >= bin_edges_h[0] && x <= bin_edges_h[ne - 1]))
+                return fail(SURR_E_INVALID_ARG, "cutoff outside [first edge, last edge]");
+            // Share of each bin's mass at or above x: the first bin lies wholly below any
+            // admissible cutoff and the last wholly above it; interior bin (lo, hi] is
+            // log-uniform, so the share above an inner x is ln(hi / x) / ln(hi / lo).
+            w.w[0][1 + c] = 0.f;
+            w.w[n_bins - 1][1 + c] = 1.f;
+            for (int b = 1; b < n_bins - 1; ++b) {
+                const double lo = bin_edges_h[b - 1], hi = bin_edges_h[b];
+                double share;
+                if (x <= lo) share = 1.0;
+                else if (x >= hi) share = 0.0;
+                else share = (std::log(hi) - std::log(x)) / (std::log(hi) - std::log(lo));
+                w.w[b][1 + c] = (float)share;
+            }
+        }
+    }
+    SURR_HIP(surr::launch_forecast_head(probs_d, n, n_bins, w, n_cutoffs, expected_speedup_d,
+                                        n_cutoffs > 0 ? discovery_d : nullptr, stream));
     return SURR_OK;
 }
 

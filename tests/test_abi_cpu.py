@@ -23,7 +23,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = B.lib()
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B.EXPORTS)
@@ -68,6 +68,45 @@ def test_select_rejects_bad_arguments_synchronously():
     assert L.surrogate_select(p, 4, 7, 0.5, 0, p, p, p, None) == B.SURR_E_INVALID_ARG
     assert L.surrogate_select(p, 4, 1, 0.5, -1, p, p, p, None) == B.SURR_E_INVALID_ARG
     assert L.surrogate_select(None, 4, 0, 0.5, 0, p, p, p, None) == B.SURR_E_INVALID_ARG
+
+
+def test_top_score_select_rejects_negative_k():
+    L = B.lib()
+    p = ctypes.c_void_p(16)
+    assert L.surrogate_select(p, 4, 2, 0.0, -1, p, p, p, None) == B.SURR_E_INVALID_ARG
+
+
+def test_forecast_head_rejects_bad_arguments_synchronously():
+    L = B.lib()
+    p = ctypes.c_void_p(256)
+    m = np.arange(1, 9, dtype=np.float64)
+    e = 2.0 ** np.array([-2, -1, -0.5, 0, 0.5, 1, 2])
+    md, ed = m.ctypes.data, e.ctypes.data
+
+    def call(n=4, nb=8, m_=md, e_=ed, cut=(1.5,), nc=None, probs=p):
+        c = np.asarray(cut, np.float64)
+        nc = c.size if nc is None else nc
+        return L.surrogate_forecast_head(probs, n, nb, m_, e_, c.ctypes.data if c.size else None,
+                                         nc, p, p, None)
+
+    assert call(n=-1) == B.SURR_E_INVALID_ARG
+    assert call(nb=0) == B.SURR_E_INVALID_ARG
+    assert call(nb=17) == B.SURR_E_INVALID_ARG
+    assert call(cut=tuple(range(9)), nc=9) == B.SURR_E_INVALID_ARG
+    assert call(m_=None) == B.SURR_E_INVALID_ARG
+    assert call(probs=None) == B.SURR_E_INVALID_ARG
+    assert call(e_=None) == B.SURR_E_INVALID_ARG
+    assert call(cut=(0.2,)) == B.SURR_E_INVALID_ARG       # below the first edge
+    assert call(cut=(4.5,)) == B.SURR_E_INVALID_ARG       # above the last edge
+    assert call(cut=(float("nan"),)) == B.SURR_E_INVALID_ARG
+    bad_e = e.copy()
+    bad_e[3] = bad_e[2]
+    assert call(e_=bad_e.ctypes.data) == B.SURR_E_INVALID_ARG
+    bad_m = m.copy()
+    bad_m[5] = np.inf
+    assert call(m_=bad_m.ctypes.data) == B.SURR_E_INVALID_ARG
+    assert call(nb=1, cut=(1.0,)) == B.SURR_E_INVALID_ARG
+    assert b"cutoff" in L.surrogate_last_error() or L.surrogate_last_error()
 
 
 def test_score_pairs_rejects_null_model():

@@ -16,7 +16,7 @@ from oracle import transformer as ot
 from paper_2605_31464_amd import binding as B
 from paper_2605_31464_amd import synth
 
-from conftest import arch_of
+from conftest import arch_of, assert_selection_near_oracle, assert_selection_valid
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -117,10 +117,13 @@ def test_tiny_config_matches_oracle(tiny):
     tok, L = synth.make_prompts(w)
     vid = synth.verdict_ids(w)
     out = scorer.score(tok, L, vid)
-    assert_parity(out, oracle_for(w.shape, W, tok, L, vid), TOL["f32"])
+    ref = oracle_for(w.shape, W, tok, L, vid)
+    assert_parity(out, ref, TOL["f32"])
     d, a, c = B.surrogate_select(out["confidence"], B.SURR_SELECT_THRESHOLD, threshold=w.select[1])
-    rd, ra = osel.select_threshold(out["confidence"].cpu().numpy(), w.select[1])
-    assert np.array_equal(d.cpu().numpy()[: c[0]], rd)
+    assert_selection_valid(out["confidence"].cpu().numpy(), d.cpu().numpy(), a.cpu().numpy(),
+                           c.cpu().numpy(), "threshold", tau=w.select[1])
+    assert_selection_near_oracle(d.cpu().numpy()[: int(c[0])], len(L), ref["confidence"],
+                                 TOL["f32"], tau=w.select[1])
 
 
 def test_tiny_ragged_edges_match_oracle(tiny):
@@ -249,5 +252,5 @@ def test_small_config_full_depth_sampled_prompts():
     assert_parity(out, oracle_for(w.shape, W, tok, L, vid, rows), TOL["bf16"], rows)
     k = w.budget_k
     d, a, c = B.surrogate_select(out["confidence"], B.SURR_SELECT_BUDGET, budget_k=k)
-    rd, ra = osel.select_budget(out["confidence"].cpu().numpy(), k)
-    assert np.array_equal(d.cpu().numpy()[: c[0]], rd) and len(rd) == k
+    assert_selection_valid(out["confidence"].cpu().numpy(), d.cpu().numpy(), a.cpu().numpy(),
+                           c.cpu().numpy(), "budget", k=k)
