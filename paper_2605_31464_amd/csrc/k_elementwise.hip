@@ -290,72 +290,178 @@ __global__ __launch_bounds__(256) void lse_verdict_kernel(const float* __restric
 }
 
 // ---------------------------------------------------------------- selection
-// flags[i] = 1 if candidate i is deferred.  Threshold: !(q_i >= tau).  Budget: the rank
-// of i in the order (NaN first, confidence ascending, index ascending) is below k.  Top
-// score: the rank of i in the order (score descending, NaN last, index ascending) is
-// below k; that is the budget order on the key -score with NaN mapped to +inf.
-__global__ __launch_bounds__(256) void select_flags_kernel(const float* __restrict__ q, int n,
-                                                           int mode, float tau, int k,
-                                                           int32_t* __restrict__ flags) {
-    __shared__ float keys[256];
-    const int tid = threadIdx.x;
-    const int i = blockIdx.x * 256 + tid;
-    const float qi = i < n ? q[i] : 0.f;
-    if (mode == 0) {
-        if (i < n) flags[i] = !(qi >= tau);
-        return;
-    }
-    const bool top = mode == 2;
-    const float ki = __builtin_isnan(qi) ? (top ? INFINITY : -INFINITY) : (top ? -qi : qi);
-    int rank = 0;
-    for (int j0 = 0; j0 < n; j0 += 256) {
-        __syncthreads();
-        const int j = j0 + tid;
-        const float qj = j < n ? q[j] : 0.f;
-        keys[tid] = __builtin_isnan(qj) ? (top ? INFINITY : -INFINITY) : (top ? -qj : qj);
-        __syncthreads();
-        const int lim = min(256, n - j0);
-        for (int jj = 0; jj < lim; ++jj) {
-            const float kj = keys[jj];
-            rank += (kj < ki) || (kj == ki && j0 + jj < i);
-        }
-    }
-    if (i < n) flags[i] = rank < k;
+// One workgroup of 1024 threads selects and compacts n <= 65536 candidates.  With
+// P = ceil(n / 1024) <= 64, wave w owns the contiguous segment [64 P w, 64 P (w + 1)) and
+// holds it in registers as P chunks of 64 consecutive candidates (lane l of chunk c is
+// candidate 64 P w + 64 c + l), so every load and every compacted store of a wave is
+// contiguous.  A candidate is deferred when
+//   threshold (MODE 0): !(q >= tau);
+//   budget    (MODE 1): its rank in (NaN first, q ascending, index ascending) is below k;
+//   top score (MODE 2): its rank in (score descending, NaN last, index ascending) is below k.
+// Ranked modes map each value to a 32-bit key whose unsigned order is the ranking order
+// (NaN to -inf or +inf, -0.0 to +0.0, top score negated), find the k-th smallest key by
+// a four-pass 8-bit radix select (LDS histograms in 16 lane-group copies, so lanes with
+// equal digits do not serialize on one address), then defer every key below it and the
+// first (k - #below) keys equal to it in index order.  Tie ranks and output offsets come
+// from ballots inside a wave and one exclusive scan over the 16 wave totals.
+constexpr int kSelThreads = 1024, kSelWaves = kSelThreads / 64, kSelChunks = 64,
+              kHistPitch = 257;
+
+__device__ __forceinline__ uint32_t order_key(float v) {
+    if (v == 0.f) v = 0.f;  // -0.0 and +0.0 rank as equal
+    const uint32_t u = __float_as_uint(v);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Ordered compaction in one workgroup: ballot + popcount prefix per wave, wave totals
-// through LDS, carried across 1024-element chunks.  flags may alias defer_idx: every
-// chunk reads its flags before any thread writes, and writes never pass the chunk.
-__global__ __launch_bounds__(1024) void select_compact_kernel(const int32_t* flags, int n,
-                                                              int32_t* defer_idx,
-                                                              int32_t* __restrict__ accept_idx,
-                                                              int32_t* __restrict__ counts) {
-    __shared__ int wsum[16];
+// Exclusive prefix over waves of a wave-uniform count; *total gets the sum.
+__device__ __forceinline__ uint32_t wave_exclusive_scan(uint32_t v, uint32_t* wsum,
+                                                        uint32_t* total) {
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) wsum[wave] = v;
+    __syncthreads();
+    uint32_t before = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) {
+        const uint32_t x = wsum[w];
+        before += w < wave ? x : 0u;
+        all += x;
+    }
+    __syncthreads();  // wsum is reused by the next scan
+    *total = all;
+    return before;
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ q, int n,
+                                                             float tau, int k,
+                                                             int32_t* __restrict__ defer_idx,
+                                                             int32_t* __restrict__ accept_idx,
+                                                             int32_t* __restrict__ counts) {
+    __shared__ uint32_t hist[16 * kHistPitch];
+    __shared__ uint32_t wsum[kSelWaves];
+    __shared__ uint32_t sel[2];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    int carry = 0;
-    for (int i0 = 0; i0 < n; i0 += 1024) {
-        const int i = i0 + tid;
-        const int f = i < n ? flags[i] : 0;
-        const uint64_t m = __ballot(f != 0);
-        const int pre = __popcll(m & ((1ull << lane) - 1ull));
-        if (lane == 0) wsum[wave] = __popcll(m);
-        __syncthreads();
-        int wpre = 0, tot = 0;
-        for (int w = 0; w < 16; ++w) {
-            wpre += w < wave ? wsum[w] : 0;
-            tot += wsum[w];
+    const int P = (n + kSelThreads - 1) / kSelThreads;
+    const int seg = wave * 64 * P + lane;  // candidate of chunk c is seg + 64 c
+    const uint64_t below = (1ull << lane) - 1ull;
+
+    // Slots past n hold kNone, above every ranked key (the largest, +inf, maps to
+    // 0xff800000) and distinct from the threshold flags 0/1, so they are never deferred,
+    // never tie with the k-th key and sort after every candidate.
+    constexpr uint32_t kNone = 0xffffffffu;
+    uint32_t key[kSelChunks];
+#pragma unroll
+    for (int c = 0; c < kSelChunks; ++c) {
+        key[c] = kNone;
+        if (c < P) {
+            const int i = seg + 64 * c;
+            if (i < n) {
+                const float v = q[i];
+                if (MODE == 0) key[c] = !(v >= tau);
+                else if (MODE == 1) key[c] = order_key(__builtin_isnan(v) ? -INFINITY : v);
+                else key[c] = order_key(__builtin_isnan(v) ? INFINITY : -v);
+            }
         }
-        const int before = carry + wpre + pre;  // deferred candidates with index < i
-        if (i < n) {
-            if (f) defer_idx[before] = i;
-            else accept_idx[i - before] = i;
+    }
+
+    uint32_t kth = 0, take = 0;  // defer keys < kth, and the first `take` keys == kth
+    if (MODE != 0 && k > 0 && k < n) {
+        uint32_t prefix = 0, pmask = 0, r = (uint32_t)(k - 1);
+        for (int pass = 0; pass < 4; ++pass) {
+            const int shift = 24 - 8 * pass;
+            for (int j = tid; j < 16 * kHistPitch; j += kSelThreads) hist[j] = 0u;
+            __syncthreads();
+            uint32_t* h = hist + (lane & 15) * kHistPitch;
+            // rank r < n lies among the candidates, so counting the kNone slots (all in
+            // the top bins) does not move the k-th key
+#pragma unroll
+            for (int c = 0; c < kSelChunks; ++c)
+                if (c < P && (key[c] & pmask) == prefix) atomicAdd(&h[(key[c] >> shift) & 255u], 1u);
+            __syncthreads();
+            if (tid < 64) {
+                uint32_t b4[4], sum = 0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    uint32_t x = 0;
+                    for (int cp = 0; cp < 16; ++cp) x += hist[cp * kHistPitch + 4 * lane + e];
+                    b4[e] = x;
+                    sum += x;
+                }
+                uint32_t incl = sum;
+#pragma unroll
+                for (int o = 1; o < 64; o <<= 1) {
+                    const uint32_t t = __shfl_up(incl, o, 64);
+                    if (lane >= o) incl += t;
+                }
+                uint32_t c0 = incl - sum;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if (r >= c0 && r < c0 + b4[e]) {
+                        sel[0] = 4 * lane + e;
+                        sel[1] = r - c0;
+                    }
+                    c0 += b4[e];
+                }
+            }
+            __syncthreads();
+            prefix |= sel[0] << shift;
+            pmask |= 255u << shift;
+            r = sel[1];
         }
-        carry += tot;
-        __syncthreads();
+        kth = prefix;
+        take = r + 1;
+    }
+
+    // Deferred count of the wave, then offsets, then the flags again in index order while
+    // storing.  Ranked modes with 0 < k < n: a wave defers its keys below the k-th and, of
+    // its keys equal to it, those whose tie rank (ties in earlier waves first) is below take.
+    const bool ranked = MODE != 0 && k > 0 && k < n;
+    const bool all = MODE != 0 && k >= n;
+    uint32_t nf = 0, seen = 0;
+    if (ranked) {
+        uint32_t nless = 0, neq = 0, unused;
+#pragma unroll
+        for (int c = 0; c < kSelChunks; ++c) {
+            if (c < P) {
+                nless += __popcll(__ballot(key[c] < kth));
+                neq += __popcll(__ballot(key[c] == kth));
+            }
+        }
+        seen = wave_exclusive_scan(neq, wsum, &unused);  // ties in earlier waves
+        const int left = max(0, (int)take - (int)seen);
+        nf = nless + (uint32_t)min(left, (int)neq);
+    } else {
+#pragma unroll
+        for (int c = 0; c < kSelChunks; ++c)
+            if (c < P) nf += __popcll(__ballot(MODE == 0 ? key[c] == 1u : (all && key[c] != kNone)));
+    }
+    uint32_t n_defer;
+    uint32_t j = wave_exclusive_scan(nf, wsum, &n_defer);  // deferred before this wave
+#pragma unroll
+    for (int c = 0; c < kSelChunks; ++c) {
+        if (c < P) {
+            bool f;
+            if (ranked) {
+                const bool eq = key[c] == kth;
+                const uint64_t em = __ballot(eq);
+                f = key[c] < kth || (eq && seen + __popcll(em & below) < take);
+                seen += __popcll(em);
+            } else {
+                f = MODE == 0 ? key[c] == 1u : (all && key[c] != kNone);
+            }
+            const uint64_t fb = __ballot(f);
+            const int i = seg + 64 * c;
+            if (i < n) {
+                const int pos = (int)(j + __popcll(fb & below));
+                if (f) defer_idx[pos] = i;
+                else accept_idx[i - pos] = i;
+            }
+            j += __popcll(fb);
+        }
     }
     if (tid == 0) {
-        counts[0] = carry;
-        counts[1] = n - carry;
+        counts[0] = (int32_t)n_defer;
+        counts[1] = n - (int32_t)n_defer;
     }
 }
 
@@ -429,13 +535,15 @@ hipError_t launch_lse_verdict(const float* logits, int64_t ld, int B, int V, con
     return hipGetLastError();
 }
 
-hipError_t launch_select(const float* conf, int n, int mode, float tau, int k, int32_t* flags,
-                         int32_t* defer_idx, int32_t* accept_idx, int32_t* counts,
-                         hipStream_t s) {
-    select_flags_kernel<<<blocks_for(n, 256), 256, 0, s>>>(conf, n, mode, tau, k, flags);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    select_compact_kernel<<<1, 1024, 0, s>>>(flags, n, defer_idx, accept_idx, counts);
+hipError_t launch_select(const float* conf, int n, int mode, float tau, int k, int32_t* defer_idx,
+                         int32_t* accept_idx, int32_t* counts, hipStream_t s) {
+    if (n < 1 || n > kSelThreads * kSelChunks || k < 0) return hipErrorInvalidValue;
+    if (mode == 0)
+        select_kernel<0><<<1, kSelThreads, 0, s>>>(conf, n, tau, k, defer_idx, accept_idx, counts);
+    else if (mode == 1)
+        select_kernel<1><<<1, kSelThreads, 0, s>>>(conf, n, tau, k, defer_idx, accept_idx, counts);
+    else
+        select_kernel<2><<<1, kSelThreads, 0, s>>>(conf, n, tau, k, defer_idx, accept_idx, counts);
     return hipGetLastError();
 }
 

@@ -47,11 +47,11 @@ hipError_t launch_lse_verdict(const float* logits, int64_t ld, int B, int V, con
                               int nv, float* lp, float* probs, float* conf, int32_t* verdict,
                               hipStream_t s);
 
-// Selection: flags then ordered compaction.  mode 0: defer !(q >= tau); mode 1: defer the
-// k lowest (NaN first); mode 2: defer the k highest (NaN last); ties by ascending index.
-hipError_t launch_select(const float* conf, int n, int mode, float tau, int k, int32_t* flags,
-                         int32_t* defer_idx, int32_t* accept_idx, int32_t* counts,
-                         hipStream_t s);
+// Selection and ordered compaction in one workgroup, 1 <= n <= 65536.  mode 0: defer
+// !(q >= tau); mode 1: defer the k lowest (NaN first); mode 2: defer the k highest (NaN
+// last); ties by ascending index.
+hipError_t launch_select(const float* conf, int n, int mode, float tau, int k, int32_t* defer_idx,
+                         int32_t* accept_idx, int32_t* counts, hipStream_t s);
 
 // ---- k_forecast.hip
 constexpr int kMaxBins = 16, kMaxCutoffs = 8;

@@ -517,8 +517,8 @@ surrogate_status surrogate_select(const float* confidence_d, int32_t n, surrogat
     if (ranked && budget_k < 0) return fail(SURR_E_INVALID_ARG, "budget_k must be >= 0");
     const int k = ranked ? std::min(budget_k, n) : 0;
     const int kmode = mode == SURR_SELECT_THRESHOLD ? 0 : mode == SURR_SELECT_BUDGET ? 1 : 2;
-    SURR_HIP(surr::launch_select(confidence_d, n, kmode, threshold, k, defer_idx_d, defer_idx_d,
-                                 accept_idx_d, counts_d, stream));
+    SURR_HIP(surr::launch_select(confidence_d, n, kmode, threshold, k, defer_idx_d, accept_idx_d,
+                                 counts_d, stream));
     return SURR_OK;
 }
 

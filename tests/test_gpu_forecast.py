@@ -86,6 +86,11 @@ def score_cases():
             s[rng.integers(0, n, max(1, n // 20))] = -0.0
             s[rng.integers(0, n, max(1, n // 20))] = 0.0
         yield n, s
+    for n in (1024, 1025, 65535):
+        yield n, rng.gamma(2.0, 0.7, n).astype(np.float32)
+    yield 3000, np.full(3000, 1.19, np.float32)
+    yield 100, np.full(100, np.nan, np.float32)
+    yield 20000, (rng.integers(-3, 9, 20000) / 4).astype(np.float32)
 
 
 @pytest.mark.parametrize("n,s", list(score_cases()), ids=lambda x: str(x) if np.isscalar(x) else "")

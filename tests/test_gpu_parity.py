@@ -82,6 +82,12 @@ def select_cases():
             q[rng.integers(0, n, max(1, n // 20))] = -0.0
             q[rng.integers(0, n, max(1, n // 20))] = 0.0
         yield n, q
+    # one run per thread boundary, all-equal and all-NaN vectors, many exact ties
+    for n in (1024, 1025, 65535):
+        yield n, rng.random(n).astype(np.float32)
+    yield 3000, np.full(3000, 0.5, np.float32)
+    yield 100, np.full(100, np.nan, np.float32)
+    yield 20000, (rng.integers(0, 7, 20000) / 8).astype(np.float32)
 
 
 @pytest.mark.parametrize("n,q", list(select_cases()), ids=lambda x: str(x) if np.isscalar(x) else "")
