@@ -88,6 +88,109 @@ def phase_rates(s, L: np.ndarray, phases: dict, steps: int) -> dict:
     return out
 
 
+def prefix_flops(s, Lp: np.ndarray, Ls: np.ndarray, pid: np.ndarray):
+    """Algorithmic FLOPs of the shared-prefix workload: building each prefix's K/V (all
+    layers but the last in full, the last only its K/V projection) and scoring each suffix
+    against its prefix (suffix rows attend every prefix key and their causal suffix keys;
+    the final layer pruned as in flops_per_prompt)."""
+    d, dq, dkv, ff, nl = s.d_model, s.d_q, s.d_kv, s.d_ff, s.n_layers
+    c_lin = 2 * d * (dq + 2 * dkv) + 2 * dq * d + 6 * d * ff
+    qh = 2 * s.n_q_heads * s.head_dim
+    Lp = Lp.astype(np.float64)
+    Ls = Ls.astype(np.float64)
+    P = Lp[pid]
+    build = float(((nl - 1) * (c_lin * Lp + qh * Lp * (Lp + 1)) + 4 * d * dkv * Lp).sum())
+    score = float(((nl - 1) * (c_lin * Ls + qh * (2 * P * Ls + Ls * (Ls + 1))) + 4 * d * dkv * Ls
+                   + (c_lin - 4 * d * dkv) + 2 * qh * (P + Ls) + 2 * d * s.vocab).sum())
+    return build, score
+
+
+def prefix_reuse_rates(B, torch, dev, model, steps: int, warmup: int) -> dict:
+    """Shared-prefix workload (every candidate of a task shares that task's prompt prefix):
+    per step, build the prefixes' K/V and score every candidate's suffix against it, then
+    the budget selection; beside it the plain path on the concatenated prompts."""
+    from paper_2605_31464_amd import synth
+    w = synth.PREFIX_CONFIGS["7b-prefix"]
+    s = w.shape
+    ptok_np, Lp, stok_np, Ls, pid = synth.make_prefix_prompts(w)
+    full_np, fl = synth.concat_prompts(ptok_np, Lp, stok_np, Ls, pid)
+    vid = np.arange(s.vocab - w.n_verdict, s.vocab, dtype=np.int32)
+    nb = len(Ls)
+    ptok = torch.from_numpy(ptok_np).to(dev)
+    stok = torch.from_numpy(stok_np).to(dev)
+    ws_b = torch.empty(B.surrogate_workspace_size(model, len(Lp), int(Lp.sum()), int(Lp.max())),
+                       dtype=torch.uint8, device=dev)
+    ws_s = torch.empty(B.surrogate_workspace_size(model, nb, int(Ls.sum()), int(Ls.max())),
+                       dtype=torch.uint8, device=dev)
+    lp = torch.empty(nb, w.n_verdict, device=dev)
+    conf = torch.empty(nb, device=dev)
+    d_idx = torch.empty(nb, dtype=torch.int32, device=dev)
+    a_idx = torch.empty(nb, dtype=torch.int32, device=dev)
+    counts = torch.empty(2, dtype=torch.int32, device=dev)
+    k = int(0.2 * nb)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, n):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n / 1e3
+
+    # building the prefixes' K/V (the cache allocates its memory, so it is timed apart)
+    caches = []
+    t_build = timed(lambda: caches.append(B.surrogate_prefix_build(model, ptok, Lp, ws_b,
+                                                                   stream=stream)), steps)
+    cache = caches.pop()
+    cache_bytes = cache.nbytes()
+    for c in caches:
+        c.close()
+
+    def score():
+        B.surrogate_score_suffixes(model, cache, pid, stok, Ls, vid, ws_s, lp, conf, stream=stream)
+        B.surrogate_select(conf, B.SURR_SELECT_BUDGET, 0.0, k, d_idx, a_idx, counts, stream=stream)
+
+    t_score = timed(score, steps)
+    cache.close()
+    del ws_b, ws_s
+    full = torch.from_numpy(full_np).to(dev)
+    ws_f = torch.empty(B.surrogate_workspace_size(model, nb, int(fl.sum()), int(fl.max())),
+                       dtype=torch.uint8, device=dev)
+
+    def plain():
+        B.surrogate_score_pairs(model, full, fl, vid, ws_f, lp, conf, stream=stream)
+        B.surrogate_select(conf, B.SURR_SELECT_BUDGET, 0.0, k, d_idx, a_idx, counts, stream=stream)
+
+    t_plain = timed(plain, 1)
+    del ws_f, full
+    build, score = prefix_flops(s, Lp, Ls, pid)
+    flop_plain = float(flops_per_prompt(s, fl).sum())
+    t_pre = t_build + t_score
+    return {"workload": w.name, "n_tasks": w.n_tasks, "batch": nb,
+            "prefix_tokens": int(Lp.sum()), "suffix_tokens": int(Ls.sum()),
+            "concatenated_tokens": int(fl.sum()),
+            "lengths": {"prefix": list(w.prefix_lengths), "suffix": list(w.suffix_lengths)},
+            "cache_bytes": cache_bytes,
+            "pairs_per_s": nb / t_score, "ms_per_step": t_score * 1e3,
+            "mfma_frac_of_peak": score / t_score / PEAK_BF16,
+            "build_ms": t_build * 1e3,
+            "build_mfma_frac_of_peak": build / t_build / PEAK_BF16,
+            "pairs_per_s_with_build": nb / t_pre,
+            "plain_pairs_per_s": nb / t_plain, "plain_ms_per_step": t_plain * 1e3,
+            "plain_mfma_frac_of_peak": flop_plain / t_plain / PEAK_BF16,
+            "speedup_vs_plain": t_plain / t_score,
+            "speedup_vs_plain_with_build": t_plain / t_pre,
+            "concatenated_tokens_per_s": float(fl.sum()) / t_score,
+            "note": "pairs_per_s scores every candidate against the resident prefix cache "
+                    "(a search reuses a task's prefix across steps); _with_build adds one "
+                    "prefix build per batch; plain scores the concatenated prompts"}
+
+
 def forecast_head_rates(B, torch, dev, n: int = 65536, reps: int = 200) -> dict:
     """Latency and achieved HBM rate of the eight-bin forecast head (expected speedup and
     three discovery cutoffs) and of top-quarter selection by expected speedup, on n
@@ -187,6 +290,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the per-phase HIP-event timing (the roofline block)")
+    ap.add_argument("--no-prefix", action="store_true",
+                    help="skip the shared-prefix workload (7B shape only)")
     ap.add_argument("--no-forecast-head", action="store_true",
                     help="skip timing the eight-bin forecast head and top-score selection")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -311,6 +416,12 @@ def main() -> int:
         out["phase_rates"] = phase_rates(s, L.astype(np.int64), phases, args.steps)
     if not args.no_forecast_head:
         out["forecast_head"] = forecast_head_rates(B, torch, dev)
+    if not args.no_prefix and args.config == "7b":
+        print("[bench] shared-prefix workload", file=sys.stderr, flush=True)
+        del ws
+        torch.cuda.empty_cache()
+        out["prefix_reuse"] = prefix_reuse_rates(B, torch, dev, model, max(1, min(args.steps, 3)),
+                                                 1)
     if not args.no_cpu_baseline:
         print("[bench] timing the float64 oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(s, W, tok_np, L, vid)

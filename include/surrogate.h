@@ -59,6 +59,9 @@ typedef enum {
 
 typedef struct surrogate_model surrogate_model; /* opaque: device weights + RoPE table */
 
+/* opaque: keys and values of every layer for a set of shared prompt prefixes */
+typedef struct surrogate_prefix_cache surrogate_prefix_cache;
+
 /* Architecture of the decoder: pre-norm RMSNorm, rotate-half RoPE, causal grouped-
  * query attention (query head a reads kv head floor(a * n_kv_heads / n_q_heads)),
  * SwiGLU MLP, final RMSNorm and an untied LM head, no biases.
@@ -130,6 +133,48 @@ surrogate_status surrogate_score_pairs(surrogate_model *m, const int32_t *tokens
                                        float *confidence_d, int32_t *verdict_d,
                                        hipStream_t stream);
 
+/* Shared prefixes.  In the paper's workload every candidate of a task is scored in a prompt
+ * that starts with the same system prompt and the task's one reference kernel (Section 3.2:
+ * each candidate is compared against its task's single reference) and ends with the
+ * candidate kernel.  That prefix is computed once: surrogate_prefix_build runs the
+ * decoder over n_prefix prefixes (laid out like the prompts of surrogate_score_pairs:
+ * tokens_d [n_prefix, row_stride], lengths_h[g] in [1, min(row_stride, max_pos - 1)],
+ * a workspace of surrogate_workspace_size(m, n_prefix, sum of lengths, max length)) and
+ * keeps every layer's keys (after RoPE) and values in a new cache, which owns its device
+ * memory (n_layers * 2 * sum_g roundup(lengths_h[g], 64) * d_kv elements of the model's
+ * dtype; surrogate_prefix_cache_bytes reports it).  The cache is ready for use once
+ * `stream` has passed the build's work; it is read-only afterwards.
+ * Errors: SURR_E_INVALID_ARG, SURR_E_SHAPE, SURR_E_WORKSPACE, SURR_E_OOM, SURR_E_HIP. */
+surrogate_status surrogate_prefix_build(surrogate_model *m, const int32_t *tokens_d,
+                                        int64_t row_stride, const int32_t *lengths_h,
+                                        int32_t n_prefix, void *workspace_d,
+                                        size_t workspace_bytes, hipStream_t stream,
+                                        surrogate_prefix_cache **out);
+
+/* As surrogate_score_pairs for prompts that continue cached prefixes: prompt i is prefix
+ * prefix_id_h[i] (or nothing, for -1) followed by its lengths_h[i] tokens in tokens_d.
+ * Every output equals that of surrogate_score_pairs on the concatenated prompt, up to
+ * rounding order.  Positions continue after the prefix, so prefix length + lengths_h[i]
+ * <= max_pos.  Workspace: surrogate_workspace_size(m, batch, sum of lengths_h, max of
+ * lengths_h).  The cache must come from the same model.
+ * Errors as surrogate_score_pairs; SURR_E_INVALID_ARG for a prefix id outside
+ * [-1, n_prefix) or a cache of another model. */
+surrogate_status surrogate_score_suffixes(surrogate_model *m, const surrogate_prefix_cache *cache,
+                                          const int32_t *prefix_id_h, const int32_t *tokens_d,
+                                          int64_t row_stride, const int32_t *lengths_h,
+                                          int32_t batch, const int32_t *verdict_ids_h,
+                                          int32_t n_verdict, void *workspace_d,
+                                          size_t workspace_bytes, float *logprobs_d,
+                                          float *probs_d, float *confidence_d, int32_t *verdict_d,
+                                          hipStream_t stream);
+
+/* Device bytes held by the cache. */
+surrogate_status surrogate_prefix_cache_bytes(const surrogate_prefix_cache *cache, size_t *bytes);
+
+/* Release the cache's device memory; pending work that reads it must have completed.
+ * NULL is ignored. */
+void surrogate_prefix_free(surrogate_prefix_cache *cache);
+
 /* Selective deferral on a device score vector confidence_d[n], 1 <= n <= 65536.  The
  * first list ("defer") is always the set sent to measurement on the device.
  *  SURR_SELECT_THRESHOLD: accept i iff confidence[i] >= threshold in float32 (the
@@ -179,7 +224,8 @@ surrogate_status surrogate_forecast_head(const float *probs_d, int64_t n, int32_
  * SURR_E_TOKEN_RANGE if an out-of-range token id was seen since the last check. */
 surrogate_status surrogate_device_status(surrogate_model *m, hipStream_t stream);
 
-/* Measurement hook.  Kernel phases of surrogate_score_pairs: */
+/* Measurement hook.  Kernel phases of surrogate_score_pairs, surrogate_prefix_build and
+ * surrogate_score_suffixes: */
 typedef enum {
     SURR_PHASE_EMBED = 0,     /* varlen token packing + embedding gather          */
     SURR_PHASE_RMSNORM,       /* RMSNorm over all tokens (attention, MLP)          */
@@ -192,6 +238,7 @@ typedef enum {
     SURR_PHASE_LAST_ROWS,     /* final layer's row-pruned work + final RMSNorm     */
     SURR_PHASE_LM_HEAD,       /* last-position LM head GEMM                        */
     SURR_PHASE_LSE_VERDICT,   /* full-vocab log-softmax + verdict read-out         */
+    SURR_PHASE_PREFIX_CAPTURE, /* surrogate_prefix_build: copy of each layer's K/V  */
     SURR_N_PHASES
 } surrogate_phase;
 

@@ -28,9 +28,10 @@ EXPORTS = ("surrogate_tensor_count", "surrogate_tensor_shape", "surrogate_load_w
            "surrogate_get_config", "surrogate_workspace_size", "surrogate_score_pairs",
            "surrogate_select", "surrogate_device_status", "surrogate_free",
            "surrogate_status_string", "surrogate_last_error", "surrogate_profile_enable",
-           "surrogate_profile_collect", "surrogate_forecast_head")
+           "surrogate_profile_collect", "surrogate_forecast_head", "surrogate_prefix_build",
+           "surrogate_score_suffixes", "surrogate_prefix_cache_bytes", "surrogate_prefix_free")
 PHASES = ("embed", "rmsnorm", "gemm_qkv", "rope", "attention", "gemm_o", "gemm_gate_up",
-          "gemm_down", "last_rows", "lm_head", "lse_verdict")
+          "gemm_down", "last_rows", "lm_head", "lse_verdict", "prefix_capture")
 
 
 class SurrogateError(RuntimeError):
@@ -76,6 +77,10 @@ def lib() -> ctypes.CDLL:
         "surrogate_profile_enable": (I32, [P, I32]),
         "surrogate_profile_collect": (I32, [P, P, P]),
         "surrogate_forecast_head": (I32, [P, I64, I32, P, P, P, I32, P, P, P]),
+        "surrogate_prefix_build": (I32, [P, P, I64, P, I32, P, SZ, P, ctypes.POINTER(P)]),
+        "surrogate_score_suffixes": (I32, [P, P, P, P, I64, P, I32, P, I32, P, SZ, P, P, P, P, P]),
+        "surrogate_prefix_cache_bytes": (I32, [P, ctypes.POINTER(SZ)]),
+        "surrogate_prefix_free": (None, [P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -193,6 +198,72 @@ def surrogate_score_pairs(model: Model, tokens, lengths, verdict_ids, workspace,
         ptr(verdict), ctypes.c_void_p(_stream(stream))), "surrogate_score_pairs")
 
 
+class PrefixCache:
+    """Owns a surrogate_prefix_cache handle (device keys and values of shared prefixes)."""
+
+    def __init__(self, handle: int, lengths):
+        self.handle = ctypes.c_void_p(handle)
+        self.lengths = list(int(x) for x in lengths)
+
+    def nbytes(self) -> int:
+        out = ctypes.c_size_t()
+        _check(lib().surrogate_prefix_cache_bytes(self.handle, ctypes.byref(out)),
+               "surrogate_prefix_cache_bytes")
+        return out.value
+
+    def close(self):
+        if self.handle:
+            lib().surrogate_prefix_free(self.handle)
+            self.handle = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def surrogate_prefix_build(model: Model, tokens, lengths, workspace, stream=None) -> PrefixCache:
+    """tokens: int32 device [G, S]; lengths: host ints; workspace: device byte tensor."""
+    import torch
+    if tokens.dtype != torch.int32 or tokens.dim() != 2 or not tokens.is_contiguous():
+        raise ValueError("tokens must be a contiguous int32 [G, S] device tensor")
+    L = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
+    G = int(tokens.shape[0])
+    if L.shape != (G,):
+        raise ValueError("lengths must have one entry per row of tokens")
+    h = ctypes.c_void_p()
+    _check(lib().surrogate_prefix_build(
+        model.handle, ctypes.c_void_p(tokens.data_ptr()), int(tokens.shape[1]),
+        L.ctypes.data_as(ctypes.c_void_p), G, ctypes.c_void_p(workspace.data_ptr()),
+        workspace.numel() * workspace.element_size(), ctypes.c_void_p(_stream(stream)),
+        ctypes.byref(h)), "surrogate_prefix_build")
+    return PrefixCache(h.value, L)
+
+
+def surrogate_score_suffixes(model: Model, cache: PrefixCache, prefix_ids, tokens, lengths,
+                             verdict_ids, workspace, logprobs, confidence, probs=None,
+                             verdict=None, stream=None):
+    """As surrogate_score_pairs for prompts = cached prefix prefix_ids[i] (-1: none) +
+    row i of tokens."""
+    import torch
+    if tokens.dtype != torch.int32 or tokens.dim() != 2 or not tokens.is_contiguous():
+        raise ValueError("tokens must be a contiguous int32 [B, S] device tensor")
+    L = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
+    pid = np.ascontiguousarray(np.asarray(prefix_ids, dtype=np.int32))
+    vid = np.ascontiguousarray(np.asarray(verdict_ids, dtype=np.int32))
+    B = int(tokens.shape[0])
+    if L.shape != (B,) or pid.shape != (B,):
+        raise ValueError("lengths and prefix_ids must have one entry per row of tokens")
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
+    _check(lib().surrogate_score_suffixes(
+        model.handle, cache.handle, pid.ctypes.data_as(ctypes.c_void_p), ptr(tokens),
+        int(tokens.shape[1]), L.ctypes.data_as(ctypes.c_void_p), B,
+        vid.ctypes.data_as(ctypes.c_void_p), int(vid.size), ptr(workspace),
+        workspace.numel() * workspace.element_size(), ptr(logprobs), ptr(probs), ptr(confidence),
+        ptr(verdict), ctypes.c_void_p(_stream(stream))), "surrogate_score_suffixes")
+
+
 def surrogate_select(confidence, mode: int, threshold: float = 0.0, budget_k: int = 0,
                      defer_idx=None, accept_idx=None, counts=None, stream=None):
     """Returns (defer_idx, accept_idx, counts) device int32 tensors."""
@@ -290,4 +361,27 @@ class Scorer:
                "verdict": torch.empty(B, dtype=torch.int32, device=self.device)}
         surrogate_score_pairs(self.model, tok, L, verdict_ids, ws, out["logprobs"], out["confidence"],
                               out["p"], out["verdict"])
+        return out
+
+    def build_prefixes(self, tokens, lengths) -> PrefixCache:
+        torch = self.torch
+        tok = torch.as_tensor(np.asarray(tokens, np.int32)).to(self.device) \
+            if not isinstance(tokens, torch.Tensor) else tokens
+        L = np.asarray(lengths, np.int32)
+        ws = self.ensure_workspace(len(L), int(L.sum()), int(L.max()))
+        return surrogate_prefix_build(self.model, tok, L, ws)
+
+    def score_suffixes(self, cache: PrefixCache, prefix_ids, tokens, lengths, verdict_ids):
+        torch = self.torch
+        tok = torch.as_tensor(np.asarray(tokens, np.int32)).to(self.device) \
+            if not isinstance(tokens, torch.Tensor) else tokens
+        L = np.asarray(lengths, np.int32)
+        B, nv = len(L), len(verdict_ids)
+        ws = self.ensure_workspace(B, int(L.sum()), int(L.max()))
+        out = {"logprobs": torch.empty(B, nv, dtype=torch.float32, device=self.device),
+               "p": torch.empty(B, nv, dtype=torch.float32, device=self.device),
+               "confidence": torch.empty(B, dtype=torch.float32, device=self.device),
+               "verdict": torch.empty(B, dtype=torch.int32, device=self.device)}
+        surrogate_score_suffixes(self.model, cache, prefix_ids, tok, L, verdict_ids, ws,
+                                 out["logprobs"], out["confidence"], out["p"], out["verdict"])
         return out

@@ -22,6 +22,11 @@
 // maximum grows by more than 2^8 (probabilities stay below 256, well inside fp32 and bf16
 // range), which is exact up to rounding because numerator and denominator share the base.
 //
+// Shared prefixes: a prompt that continues a cached prefix of Lp tokens first walks the
+// ceil(Lp / 64) tiles of that prefix's cached K and V^T (every query sees every prefix
+// key; only the padding past Lp is masked), then its own keys with the causal mask as
+// above.
+//
 // fp32 path: one thread per query row, exact expf, for the float32 model.
 #include "common.h"
 #include "kernels.h"
@@ -88,14 +93,36 @@ struct AttnDma {
         for (int i = 0; i < HALF; ++i)
             dma_load_16B_sbase(vb, voff[i], w + (HALF + i) * 256u * 16u);
     }
+
+    // A tile of a cached prefix: same LDS placement, the cache's own leading dimensions
+    // (offsets formed per tile), never clamped (prefix blocks are whole 64-row tiles).
+    __device__ __forceinline__ void issue_prefix(const uint16_t* kbase, int64_t ld_k,
+                                                 const uint16_t* vbase, int64_t ld_v, int k0,
+                                                 uint32_t stage_lds, int tid, int wave) const {
+        const uint16_t* kb = kbase + (int64_t)k0 * ld_k;
+        const uint16_t* vb = vbase + k0;
+        const uint32_t w = stage_lds + (uint32_t)wave * 64u * 16u;
+#pragma unroll
+        for (int i = 0; i < HALF; ++i) {
+            const int p = i * 256 + tid;
+            const int r = p / NCH, c = (p % NCH) ^ lds_swz<NCH>(r);
+            dma_load_16B_sbase(kb, (uint32_t)((r * ld_k + c * 8) * 2), w + i * 256u * 16u);
+        }
+#pragma unroll
+        for (int i = 0; i < HALF; ++i) {
+            const int p = i * 256 + tid;
+            const int d = p >> 3, cv = (p & 7) ^ lds_swz<8>(d);
+            dma_load_16B_sbase(vb, (uint32_t)((d * ld_v + cv * 8) * 2), w + (HALF + i) * 256u * 16u);
+        }
+    }
 };
 
-template <int HD>
+template <int HD, bool PREFIX>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
     const uint16_t* __restrict__ qkv, int64_t ld, const uint16_t* __restrict__ vt, int64_t ld_vt,
     const int32_t* __restrict__ vt_off, uint16_t* __restrict__ out, int64_t ld_out,
     const int32_t* __restrict__ cu, const int2* __restrict__ work, int n_items, int nqh, int nkvh,
-    float scale_log2) {
+    float scale_log2, PrefixKV pf) {
     constexpr int NCH = HD / 8, KCH = kBKV * NCH, CHUNKS = 2 * KCH;
     constexpr int KS = HD / 16;  // MFMA steps over the head dim for S
     constexpr int DB = HD / 32;  // 32-dim blocks of O
@@ -117,13 +144,24 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
     const uint16_t* kbase = qkv + (int64_t)start * ld + (int64_t)(nqh + kvh) * HD;
     const uint16_t* vbase = vt + (int64_t)kvh * HD * ld_vt + vt_off[wk.x];
     const uint32_t lds0 = lds_offset(lds);
+    // Cached prefix: tiles 0 .. np - 1 come from it, the prompt's own tiles follow.
+    int Lp = 0, np = 0;
+    const uint16_t* kpre = nullptr;
+    const uint16_t* vpre = nullptr;
+    if constexpr (PREFIX) {
+        Lp = pf.len[wk.x];
+        np = (Lp + kBKV - 1) / kBKV;
+        const int po = pf.off[wk.x];
+        kpre = static_cast<const uint16_t*>(pf.k) + (int64_t)po * pf.ld_k + (int64_t)kvh * HD;
+        vpre = static_cast<const uint16_t*>(pf.v) + (int64_t)kvh * HD * pf.ld_v + po;
+    }
 
     const int kv_end = min(L, q0 + kBQ);
-    const int n_tiles = (kv_end + kBKV - 1) / kBKV;
+    const int n_tiles = np + (kv_end + kBKV - 1) / kBKV;
     const int qw0 = q0 + wave * 32;  // first query row of this wavefront
     const int my_q = qw0 + l32;
-    // tiles this wavefront needs: keys up to its last valid query row
-    const int wave_tiles = qw0 < L ? min(qw0 + 31, L - 1) / kBKV + 1 : 0;
+    // tiles this wavefront needs: the prefix, then keys up to its last valid query row
+    const int wave_tiles = qw0 < L ? np + min(qw0 + 31, L - 1) / kBKV + 1 : 0;
 
     bf16x8 qf[KS];
     {
@@ -134,7 +172,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
             qf[st] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(qrow + 16 * st));
     }
     const AttnDma<HD> dma(ld, ld_vt, tid);
-    dma.issue(kbase, ld, L, vbase, 0, lds0, tid, wave);
+    auto issue_tile = [&](int t, uint32_t stage_lds) {
+        if (PREFIX && t < np)
+            dma.issue_prefix(kpre, pf.ld_k, vpre, pf.ld_v, t * kBKV, stage_lds, tid, wave);
+        else
+            dma.issue(kbase, ld, L, vbase, (t - np) * kBKV, stage_lds, tid, wave);
+    };
+    issue_tile(0, lds0);
 
     f32x16 o[DB];
 #pragma unroll
@@ -146,8 +190,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
     __syncthreads();
     for (int t = 0; t < n_tiles; ++t) {
         if (t + 1 < n_tiles)  // its stage was released by the barrier that ended tile t - 1
-            dma.issue(kbase, ld, L, vbase, (t + 1) * kBKV,
-                      lds0 + (uint32_t)((t + 1) & 1) * CHUNKS * 16u, tid, wave);
+            issue_tile(t + 1, lds0 + (uint32_t)((t + 1) & 1) * CHUNKS * 16u);
         if (t < wave_tiles) {
             const uint4* Ks = lds + (t & 1) * CHUNKS;
             const uint4* Vs = Ks + KCH;
@@ -163,9 +206,21 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
                     s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[st], s[kb], 0, 0, 0);
                 }
             }
-            const int k0 = t * kBKV;
-            if (k0 + kBKV - 1 > qw0 || k0 + kBKV > L) {  // causal / length mask
-                const int lim = lim_q - (k0 + 4 * h);
+            // keys past lim (counted from key 4 h of the tile) are masked: in a prefix tile
+            // those past the prefix; in an own tile those after the query (causal) or past
+            // the prompt
+            bool masked;  // wave-uniform
+            int lim;
+            if (PREFIX && t < np) {
+                const int k0 = t * kBKV;
+                masked = k0 + kBKV > Lp;
+                lim = Lp - 1 - (k0 + 4 * h);
+            } else {
+                const int k0 = (t - np) * kBKV;
+                masked = k0 + kBKV - 1 > qw0 || k0 + kBKV > L;
+                lim = lim_q - (k0 + 4 * h);
+            }
+            if (masked) {
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -233,12 +288,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
 // ---------------------------------------------------------------- fp32
 constexpr int kBQ32 = 64;
 
-template <int HD>
+template <int HD, bool PREFIX>
 __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ qkv, int64_t ld,
                                                       float* __restrict__ out, int64_t ld_out,
                                                       const int32_t* __restrict__ cu,
                                                       const int2* __restrict__ work, int nqh,
-                                                      int nkvh, float scale) {
+                                                      int nkvh, float scale, PrefixKV pf) {
     __shared__ float Ks[64][HD + 1];
     __shared__ float Vs[64][HD + 1];
     const int tid = threadIdx.x;
@@ -257,6 +312,33 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
         o[d] = 0.f;
     }
     float m = -INFINITY, l = 0.f;
+    if constexpr (PREFIX) {  // every key of the cached prefix, no causal mask
+        const int Lp = pf.len[wk.x], po = pf.off[wk.x];
+        const float* kp = static_cast<const float*>(pf.k) + (int64_t)po * pf.ld_k + (int64_t)kvh * HD;
+        const float* vp = static_cast<const float*>(pf.v) + (int64_t)po * pf.ld_v + (int64_t)kvh * HD;
+        for (int k0 = 0; k0 < Lp; k0 += 64) {
+            __syncthreads();
+            const int r = min(k0 + tid, Lp - 1);
+            for (int d = 0; d < HD; ++d) {
+                Ks[tid][d] = kp[(int64_t)r * pf.ld_k + d];
+                Vs[tid][d] = vp[(int64_t)r * pf.ld_v + d];
+            }
+            __syncthreads();
+            const int lim = min(64, Lp - k0);
+            for (int kk = 0; kk < lim; ++kk) {
+                float sdot = 0.f;
+#pragma unroll
+                for (int d = 0; d < HD; ++d) sdot = fmaf(q[d], Ks[kk][d], sdot);
+                const float sc = sdot * scale;
+                const float m_new = fmaxf(m, sc);
+                const float corr = expf(m - m_new), p = expf(sc - m_new);
+                l = l * corr + p;
+#pragma unroll
+                for (int d = 0; d < HD; ++d) o[d] = o[d] * corr + p * Vs[kk][d];
+                m = m_new;
+            }
+        }
+    }
     const int kv_end = min(L, q0 + kBQ32);
     for (int k0 = 0; k0 < kv_end; k0 += 64) {
         __syncthreads();
@@ -295,8 +377,10 @@ int attention_q_tile(Act t) { return t == Act::BF16 ? kBQ : kBQ32; }
 hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, const void* vt, int64_t ld_vt,
                             const int32_t* vt_off, void* out, int64_t ld_out, const int32_t* cu,
                             const int2* work, int n_items, int n_q_heads, int n_kv_heads,
-                            int head_dim, hipStream_t s) {
+                            int head_dim, hipStream_t s, const PrefixKV* pf) {
     if (n_items == 0) return hipSuccess;
+    const PrefixKV pk = pf ? *pf : PrefixKV();
+    if (pf && (!pk.k || !pk.v || !pk.len || !pk.off)) return hipErrorInvalidValue;
     if (t == Act::BF16) {
         const unsigned grid = (unsigned)((n_items + 7) / 8 * 8) * (unsigned)n_q_heads;
         const float sl2 = kLog2e / sqrtf((float)head_dim);
@@ -307,22 +391,33 @@ hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, const void* 
         if (!v || !vt_off || ld_vt % 8 || (int64_t)head_dim * ld_vt * 2 > UINT32_MAX ||
             64 * ld_qkv * 2 > UINT32_MAX)
             return hipErrorInvalidValue;
+        if (pf && (pk.ld_k % 8 || pk.ld_v % 8 || (int64_t)head_dim * pk.ld_v * 2 > UINT32_MAX ||
+                   64 * pk.ld_k * 2 > UINT32_MAX))
+            return hipErrorInvalidValue;
+#define SURR_ATTN_BF16(HD, PRE)                                                                 \
+    attn_bf16_kernel<HD, PRE><<<grid, 256, 0, s>>>(q, ld_qkv, v, ld_vt, vt_off, o, ld_out, cu, \
+                                                   work, n_items, n_q_heads, n_kv_heads, sl2, pk)
         switch (head_dim) {
-            case 64: attn_bf16_kernel<64><<<grid, 256, 0, s>>>(q, ld_qkv, v, ld_vt, vt_off, o, ld_out, cu, work, n_items, n_q_heads, n_kv_heads, sl2); break;
-            case 128: attn_bf16_kernel<128><<<grid, 256, 0, s>>>(q, ld_qkv, v, ld_vt, vt_off, o, ld_out, cu, work, n_items, n_q_heads, n_kv_heads, sl2); break;
+            case 64: if (pf) SURR_ATTN_BF16(64, true); else SURR_ATTN_BF16(64, false); break;
+            case 128: if (pf) SURR_ATTN_BF16(128, true); else SURR_ATTN_BF16(128, false); break;
             default: return hipErrorInvalidValue;
         }
+#undef SURR_ATTN_BF16
     } else {
         const unsigned grid = (unsigned)n_items * (unsigned)n_q_heads;
         const float sc = 1.f / sqrtf((float)head_dim);
         const float* q = static_cast<const float*>(qkv);
         float* o = static_cast<float*>(out);
+#define SURR_ATTN_F32(HD, PRE)                                                               \
+    attn_f32_kernel<HD, PRE><<<grid, 64, 0, s>>>(q, ld_qkv, o, ld_out, cu, work, n_q_heads, \
+                                                 n_kv_heads, sc, pk)
         switch (head_dim) {
-            case 32: attn_f32_kernel<32><<<grid, 64, 0, s>>>(q, ld_qkv, o, ld_out, cu, work, n_q_heads, n_kv_heads, sc); break;
-            case 64: attn_f32_kernel<64><<<grid, 64, 0, s>>>(q, ld_qkv, o, ld_out, cu, work, n_q_heads, n_kv_heads, sc); break;
-            case 128: attn_f32_kernel<128><<<grid, 64, 0, s>>>(q, ld_qkv, o, ld_out, cu, work, n_q_heads, n_kv_heads, sc); break;
+            case 32: if (pf) SURR_ATTN_F32(32, true); else SURR_ATTN_F32(32, false); break;
+            case 64: if (pf) SURR_ATTN_F32(64, true); else SURR_ATTN_F32(64, false); break;
+            case 128: if (pf) SURR_ATTN_F32(128, true); else SURR_ATTN_F32(128, false); break;
             default: return hipErrorInvalidValue;
         }
+#undef SURR_ATTN_F32
     }
     return hipGetLastError();
 }

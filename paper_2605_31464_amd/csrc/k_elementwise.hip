@@ -16,6 +16,7 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ 
                                                     int64_t T, const void* __restrict__ embed,
                                                     int d, int vocab, float* __restrict__ x,
                                                     int32_t* __restrict__ pos,
+                                                    const int32_t* __restrict__ pos_off,
                                                     const int32_t* __restrict__ vt_off,
                                                     int32_t* __restrict__ vcol,
                                                     int32_t* __restrict__ err_flag) {
@@ -34,7 +35,7 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ 
         tok = 0;
     }
     if (lane == 0) {
-        pos[t] = j;
+        pos[t] = pos_off ? pos_off[lo] + j : j;
         if (vcol) vcol[t] = vt_off[lo] + vt_key_order(j);
     }
     float4* xr = reinterpret_cast<float4*>(x + t * d);
@@ -231,6 +232,30 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const uint32_t* __rest
     const uint32_t* s = src + (int64_t)rows[r] * ld_src;
     uint32_t* o = dst + r * ld_dst;
     for (int c = threadIdx.x; c < words; c += 256) o[c] = s[c];
+}
+
+// Row r of a 64-row-aligned cache: prompt b = the last with po[b] <= r, j = r - po[b];
+// copies columns [col0, col0 + words) of packed row cu[b] + j when j < L_b, else zeros.
+__global__ __launch_bounds__(256) void capture_rows_kernel(const uint32_t* __restrict__ src,
+                                                           int64_t ld_src, int col0, int words,
+                                                           const int32_t* __restrict__ cu,
+                                                           const int32_t* __restrict__ po, int B,
+                                                           uint32_t* __restrict__ dst,
+                                                           int64_t ld_dst) {
+    const int64_t r = blockIdx.x;
+    int lo = 0, hi = B;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (po[mid] <= r) lo = mid; else hi = mid;
+    }
+    const int j = (int)(r - po[lo]);
+    uint32_t* o = dst + r * ld_dst;
+    if (j < cu[lo + 1] - cu[lo]) {
+        const uint32_t* sr = src + (int64_t)(cu[lo] + j) * ld_src + col0;
+        for (int c = threadIdx.x; c < words; c += 256) o[c] = sr[c];
+    } else {
+        for (int c = threadIdx.x; c < words; c += 256) o[c] = 0u;
+    }
 }
 
 // ---------------------------------------------------------------- LSE + verdicts
@@ -471,14 +496,28 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 
 hipError_t launch_embed(Act wt, const int32_t* tokens, int64_t row_stride, const int32_t* cu,
                         int B, int64_t T, const void* embed, int d, int vocab, float* x,
-                        int32_t* pos, const int32_t* vt_off, int32_t* vcol, int32_t* err_flag,
-                        hipStream_t s) {
+                        int32_t* pos, const int32_t* pos_off, const int32_t* vt_off, int32_t* vcol,
+                        int32_t* err_flag, hipStream_t s) {
     if (wt == Act::BF16)
         embed_kernel<true><<<blocks_for(T, 4), 256, 0, s>>>(tokens, row_stride, cu, B, T, embed,
-                                                            d, vocab, x, pos, vt_off, vcol, err_flag);
+                                                            d, vocab, x, pos, pos_off, vt_off, vcol,
+                                                            err_flag);
     else
         embed_kernel<false><<<blocks_for(T, 4), 256, 0, s>>>(tokens, row_stride, cu, B, T, embed,
-                                                             d, vocab, x, pos, vt_off, vcol, err_flag);
+                                                             d, vocab, x, pos, pos_off, vt_off,
+                                                             vcol, err_flag);
+    return hipGetLastError();
+}
+
+hipError_t launch_capture_rows(const void* src, int64_t ld_src, int col0, int cols, int elem_bytes,
+                               const int32_t* cu, const int32_t* po, int B, int64_t rows,
+                               void* dst, int64_t ld_dst, hipStream_t s) {
+    if (rows == 0) return hipSuccess;
+    // moved as 4-byte words: cols, col0 and both leading dimensions times elem_bytes are
+    // multiples of 4 for every caller (head_dim is even)
+    capture_rows_kernel<<<(unsigned)rows, 256, 0, s>>>(
+        static_cast<const uint32_t*>(src), ld_src * elem_bytes / 4, col0 * elem_bytes / 4,
+        cols * elem_bytes / 4, cu, po, B, static_cast<uint32_t*>(dst), ld_dst * elem_bytes / 4);
     return hipGetLastError();
 }
 

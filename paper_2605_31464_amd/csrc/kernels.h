@@ -11,13 +11,21 @@ enum class Act { F32, BF16 };  // storage type of activations and matrices
 
 // ---- k_elementwise.hip
 // Gather embedding rows of the packed tokens into the fp32 residual x[T, d] and
-// record each token's position inside its prompt.  cu[B+1] are prompt offsets.  With
-// vt_off (per-prompt first column of the transposed V copy), vcol[t] receives the token's
-// column there: vt_off[b] + vt_key_order(position).
+// record each token's position: its index j inside its prompt, plus pos_off[b] when
+// pos_off is set (tokens that continue a cached prefix).  cu[B+1] are prompt offsets.
+// With vt_off (per-prompt first column of the transposed V copy), vcol[t] receives the
+// token's column there: vt_off[b] + vt_key_order(j).
 hipError_t launch_embed(Act wt, const int32_t* tokens, int64_t row_stride, const int32_t* cu,
                         int B, int64_t T, const void* embed, int d, int vocab, float* x,
-                        int32_t* pos, const int32_t* vt_off, int32_t* vcol, int32_t* err_flag,
-                        hipStream_t s);
+                        int32_t* pos, const int32_t* pos_off, const int32_t* vt_off, int32_t* vcol,
+                        int32_t* err_flag, hipStream_t s);
+
+// Copy columns [col0, col0 + cols) of the packed rows of B prompts into a cache of
+// 64-row-aligned blocks: row j of prompt b goes to row po[b] + j; rows po[b] + L_b up to
+// the next block are zeroed (rows = po[B]).
+hipError_t launch_capture_rows(const void* src, int64_t ld_src, int col0, int cols, int elem_bytes,
+                               const int32_t* cu, const int32_t* po, int B, int64_t rows,
+                               void* dst, int64_t ld_dst, hipStream_t s);
 
 // Zero the padding columns of the transposed V copy (rows x [vt_off[b] + L_b,
 // vt_off[b + 1]) in stored order) so masked keys multiply finite values.
@@ -96,14 +104,31 @@ hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, 
                        const RopeArgs& rope = RopeArgs());
 
 // ---- k_attention.hip
+// Keys and values of shared prompt prefixes, computed once and attended by every prompt
+// that continues one.  Per layer, prefix g owns rows [off, off + roundup(len, 64)) of k
+// (keys after RoPE, [rows][ld_k], kv heads side by side) and the same range of v: bf16
+// keeps V transposed like the vt copy ([kv head * hd + dim][ld_v] columns, 16-key groups
+// in vt_key_order), fp32 keeps V rows [rows][ld_v].  Padding rows and columns are zero.
+// len[b] / off[b] give prompt b's prefix length (0: none) and its first row.
+struct PrefixKV {
+    const void* k = nullptr;
+    int64_t ld_k = 0;
+    const void* v = nullptr;
+    int64_t ld_v = 0;
+    const int32_t* len = nullptr;
+    const int32_t* off = nullptr;
+};
+
 // Causal GQA attention over the packed qkv rows.  work[i] = (prompt, q_tile) items;
 // grid = n_items * n_q_heads.  q_tile covers rows [q_tile * attention_q_tile, +tile) of
 // the prompt.  bf16 reads V from the transposed copy vt (see RopeArgs; ld_vt % 8 == 0,
-// vt_off[b] % 64 == 0); the fp32 kernel reads V from qkv and ignores vt.
+// vt_off[b] % 64 == 0); the fp32 kernel reads V from qkv and ignores vt.  With a prefix
+// (pf != nullptr), every query of prompt b also attends, before its own keys, all
+// pf->len[b] keys of its cached prefix.
 hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, const void* vt, int64_t ld_vt,
                             const int32_t* vt_off, void* out, int64_t ld_out, const int32_t* cu,
                             const int2* work, int n_items, int n_q_heads, int n_kv_heads,
-                            int head_dim, hipStream_t s);
+                            int head_dim, hipStream_t s, const PrefixKV* pf = nullptr);
 int attention_q_tile(Act t);
 
 }  // namespace surr

@@ -47,8 +47,8 @@ struct LayerW {
 
 // Byte offsets of one call's workspace regions.
 struct WsLayout {
-    size_t cu, last, vid, work, work_last, vt_off, pos, vcol, x, h, qkv, vt, o, u, gu, o_last,
-        x_last, h_last, u_last, gu_last, y, logits, total;
+    size_t cu, last, vid, work, work_last, vt_off, pfx_len, pfx_off, pos, vcol, x, h, qkv, vt, o,
+        u, gu, o_last, x_last, h_last, u_last, gu_last, y, logits, total;
     int64_t ld_vt;  // columns of the transposed V copy (bf16 models)
 };
 
@@ -121,6 +121,20 @@ struct surrogate_model {
     int64_t d_qkv() const { return d_q() + 2 * d_kv(); }
 };
 
+// Keys (after RoPE) and values of every layer for a set of shared prompt prefixes.
+// Prefix g owns rows [off[g], off[g] + roundup(len[g], 64)) of each layer's K [rows][d_kv]
+// and the same range of its V: bf16 stores V transposed ([d_kv][rows], keys of each
+// 16-key group in the order of the kernels' V^T copy), fp32 stores V rows [rows][d_kv].
+struct surrogate_prefix_cache {
+    const surrogate_model* model = nullptr;
+    std::vector<int32_t> len, off;
+    int64_t rows = 0;
+    char* mem = nullptr;
+    size_t k_bytes = 0, v_bytes = 0;  // per layer
+    void* k(int l) const { return mem + (size_t)l * (k_bytes + v_bytes); }
+    void* v(int l) const { return mem + (size_t)l * (k_bytes + v_bytes) + k_bytes; }
+};
+
 namespace {
 
 WsLayout layout(const surrogate_model* m, int64_t B, int64_t T) {
@@ -138,6 +152,8 @@ WsLayout layout(const surrogate_model* m, int64_t B, int64_t T) {
     w.work = take(8 * items);
     w.work_last = take(8 * B);
     w.vt_off = take(4 * (B + 1));
+    w.pfx_len = take(4 * B);
+    w.pfx_off = take(4 * B);
     w.pos = take(4 * T);
     // Transposed V copy: every prompt's keys start on a 64-column boundary, so its
     // padded ranges need at most T + 63 B columns.
@@ -159,6 +175,262 @@ WsLayout layout(const surrogate_model* m, int64_t B, int64_t T) {
     w.logits = take(4 * B * c.vocab);
     w.total = off;
     return w;
+}
+
+}  // namespace
+
+namespace {
+
+// What one pass over a ragged batch does besides the decoder layers.
+struct PassIO {
+    bool build = false;  // capture every layer's K/V into `capture`; no attention or MLP in
+                         // the final layer and no LM head
+    surrogate_prefix_cache* capture = nullptr;
+    const surrogate_prefix_cache* prefix = nullptr;  // prompts continue cached prefixes
+    const int32_t* prefix_id_h = nullptr;            // per prompt: prefix index or -1
+    const int32_t* verdict_ids_h = nullptr;
+    int32_t n_verdict = 0;
+    float* logprobs_d = nullptr;
+    float* probs_d = nullptr;
+    float* confidence_d = nullptr;
+    int32_t* verdict_d = nullptr;
+};
+
+surrogate_status check_verdicts(const surrogate_config& c, const int32_t* vid, int32_t n) {
+    if (n < 1 || n > 16) return fail(SURR_E_INVALID_ARG, "n_verdict must be in [1, 16]");
+    for (int i = 0; i < n; ++i) {
+        if (vid[i] < 0 || vid[i] >= c.vocab) return fail(SURR_E_INVALID_ARG, "verdict id out of range");
+        for (int j = 0; j < i; ++j)
+            if (vid[j] == vid[i]) return fail(SURR_E_INVALID_ARG, "duplicate verdict id");
+    }
+    return SURR_OK;
+}
+
+surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t row_stride,
+                          const int32_t* lengths_h, int32_t batch, void* workspace_d,
+                          size_t workspace_bytes, const PassIO& io, hipStream_t stream) {
+    const surrogate_config& c = m->cfg;
+    if (batch < 1) return fail(SURR_E_INVALID_ARG, "batch must be >= 1");
+    if (row_stride < 1) return fail(SURR_E_INVALID_ARG, "row_stride must be >= 1");
+    std::vector<int32_t> plen(batch, 0), poff(batch, 0);
+    if (io.prefix) {
+        const int np = (int)io.prefix->len.size();
+        for (int b = 0; b < batch; ++b) {
+            const int g = io.prefix_id_h[b];
+            if (g < -1 || g >= np) return fail(SURR_E_INVALID_ARG, "prefix id of prompt " + std::to_string(b) + " outside [-1, n_prefix)");
+            if (g >= 0) {
+                plen[b] = io.prefix->len[g];
+                poff[b] = io.prefix->off[g];
+            }
+        }
+    }
+    // a prompt's positions run to prefix length + length - 1 < max_pos; a prefix leaves
+    // room for at least one continuing token
+    int64_t T = 0;
+    for (int b = 0; b < batch; ++b) {
+        const int64_t cap = std::min<int64_t>(row_stride, (int64_t)c.max_pos - plen[b] - (io.build ? 1 : 0));
+        if (lengths_h[b] < 1 || lengths_h[b] > cap)
+            return fail(SURR_E_SHAPE, "length of prompt " + std::to_string(b) + (io.build ? " outside [1, min(row_stride, max_pos - 1)]" : io.prefix ? " outside [1, min(row_stride, max_pos - prefix length)]" : " outside [1, min(row_stride, max_pos)]"));
+        T += lengths_h[b];
+    }
+    if (T + 64 * (int64_t)batch > INT32_MAX)
+        return fail(SURR_E_SHAPE, "total tokens plus 64 per prompt exceed 2^31 - 1");
+    if (reinterpret_cast<uintptr_t>(workspace_d) % kAlign) return fail(SURR_E_INVALID_ARG, "workspace must be 256-byte aligned");
+    const WsLayout w = layout(m, batch, T);
+    if (workspace_bytes < w.total)
+        return fail(SURR_E_WORKSPACE, "workspace needs " + std::to_string(w.total) + " bytes");
+    const int32_t n_verdict = io.n_verdict;
+    const int32_t* verdict_ids_h = io.verdict_ids_h;
+    float* logprobs_d = io.logprobs_d;
+    float* probs_d = io.probs_d;
+    float* confidence_d = io.confidence_d;
+    int32_t* verdict_d = io.verdict_d;
+    // ---- plan: prompt offsets, last rows, verdict ids, attention work lists
+    const int qt = surr::attention_q_tile(m->act);
+    std::vector<int32_t> cu(batch + 1, 0), last(batch);
+    for (int b = 0; b < batch; ++b) {
+        cu[b + 1] = cu[b] + lengths_h[b];
+        last[b] = cu[b + 1] - 1;
+    }
+    std::vector<int32_t> vt_off(batch + 1, 0);
+    for (int b = 0; b < batch; ++b) vt_off[b + 1] = vt_off[b] + (lengths_h[b] + 63) / 64 * 64;
+    std::vector<int2> work, work_last(batch);
+    for (int b = 0; b < batch; ++b) {
+        for (int t = 0; t * qt < lengths_h[b]; ++t) work.push_back(make_int2(b, t));
+        work_last[b] = make_int2(b, (lengths_h[b] - 1) / qt);
+    }
+    // Longest key range first (a cached prefix counts in whole tiles), so the big causal
+    // tiles start early; stable for a deterministic order.
+    auto kv_len = [&](const int2& it) {
+        return (plen[it.x] + 63) / 64 * 64 + std::min(lengths_h[it.x], (it.y + 1) * qt);
+    };
+    std::stable_sort(work.begin(), work.end(),
+                     [&](const int2& a, const int2& b) { return kv_len(a) > kv_len(b); });
+
+    const size_t meta_bytes = w.pos;  // cu .. vt_off are contiguous from offset 0
+    {
+        std::lock_guard<std::mutex> lock(m->mu);
+        if (m->staged_pending) SURR_HIP(hipEventSynchronize(m->staged));
+        m->staged_pending = false;
+        if (m->pinned_bytes < meta_bytes) {
+            if (m->pinned) SURR_HIP(hipHostFree(m->pinned));
+            m->pinned = nullptr;
+            m->pinned_bytes = 0;
+            if (hipHostMalloc(&m->pinned, meta_bytes, hipHostMallocDefault) != hipSuccess)
+                return fail(SURR_E_OOM, "pinned staging buffer");
+            m->pinned_bytes = meta_bytes;
+        }
+        char* P = static_cast<char*>(m->pinned);
+        std::memcpy(P + w.cu, cu.data(), 4 * cu.size());
+        std::memcpy(P + w.last, last.data(), 4 * last.size());
+        if (n_verdict) std::memcpy(P + w.vid, verdict_ids_h, 4 * (size_t)n_verdict);
+        std::memcpy(P + w.work, work.data(), 8 * work.size());
+        std::memcpy(P + w.work_last, work_last.data(), 8 * work_last.size());
+        std::memcpy(P + w.vt_off, vt_off.data(), 4 * vt_off.size());
+        std::memcpy(P + w.pfx_len, plen.data(), 4 * plen.size());
+        std::memcpy(P + w.pfx_off, poff.data(), 4 * poff.size());
+        SURR_HIP(hipMemcpyAsync(workspace_d, P, meta_bytes, hipMemcpyHostToDevice, stream));
+        SURR_HIP(hipEventRecord(m->staged, stream));
+        m->staged_pending = true;
+    }
+
+    char* W = static_cast<char*>(workspace_d);
+    const int32_t* d_cu = reinterpret_cast<const int32_t*>(W + w.cu);
+    const int32_t* d_last = reinterpret_cast<const int32_t*>(W + w.last);
+    const int32_t* d_vid = reinterpret_cast<const int32_t*>(W + w.vid);
+    const int2* d_work = reinterpret_cast<const int2*>(W + w.work);
+    const int2* d_work_last = reinterpret_cast<const int2*>(W + w.work_last);
+    int32_t* d_pos = reinterpret_cast<int32_t*>(W + w.pos);
+    const int32_t* d_po = reinterpret_cast<const int32_t*>(W + w.vt_off);  // 64-aligned row blocks
+    const int32_t* d_pfx_len = reinterpret_cast<const int32_t*>(W + w.pfx_len);
+    const int32_t* d_pfx_off = reinterpret_cast<const int32_t*>(W + w.pfx_off);
+    const bool bf16 = m->act == Act::BF16;
+    const int32_t* d_vt_off = bf16 ? reinterpret_cast<const int32_t*>(W + w.vt_off) : nullptr;
+    int32_t* d_vcol = bf16 ? reinterpret_cast<int32_t*>(W + w.vcol) : nullptr;
+    uint16_t* vt = bf16 ? reinterpret_cast<uint16_t*>(W + w.vt) : nullptr;
+    float* x = reinterpret_cast<float*>(W + w.x);
+    void* h = W + w.h;
+    void* qkv = W + w.qkv;
+    void* o = W + w.o;
+    void* u = W + w.u;
+    float* gu = reinterpret_cast<float*>(W + w.gu);
+    void* o_last = W + w.o_last;
+    float* x_last = reinterpret_cast<float*>(W + w.x_last);
+    void* h_last = W + w.h_last;
+    void* u_last = W + w.u_last;
+    float* gu_last = reinterpret_cast<float*>(W + w.gu_last);
+    void* y = W + w.y;
+    float* logits = reinterpret_cast<float*>(W + w.logits);
+
+    const Act a = m->act;
+    const int d = c.d_model, ff = c.d_ff, nq = c.n_q_heads, nkv = c.n_kv_heads, hd = c.head_dim;
+    const int dq = (int)m->d_q(), dqkv = (int)m->d_qkv();
+    const int Ti = (int)T;
+
+
+    // Phase bracketing for the measurement hook (a no-op unless profiling is on).
+    auto mark = [&](int phase) -> hipError_t {
+        if (!m->profiling) return hipSuccess;
+        while (m->ev_used + 2 > m->ev_pool.size()) {
+            hipEvent_t e;
+            hipError_t r = hipEventCreate(&e);
+            if (r != hipSuccess) return r;
+            m->ev_pool.push_back(e);
+        }
+        m->rec.emplace_back(phase, m->ev_used);
+        const hipEvent_t e0 = m->ev_pool[m->ev_used];
+        m->ev_used += 2;
+        return hipEventRecord(e0, stream);
+    };
+    auto done = [&]() -> hipError_t {
+        if (!m->profiling) return hipSuccess;
+        return hipEventRecord(m->ev_pool[m->rec.back().second + 1], stream);
+    };
+#define SURR_PHASE_RUN(phase, expr)  \
+    do {                             \
+        SURR_HIP(mark(phase));       \
+        SURR_HIP(expr);              \
+        SURR_HIP(done());            \
+    } while (0)
+
+    auto mlp = [&](const LayerW& L, void* hin, void* uout, float* gtmp, float* xres, int M,
+                   int ph_gu, int ph_down) -> surrogate_status {
+        if (a == Act::BF16) {
+            SURR_PHASE_RUN(ph_gu, surr::launch_gemm(a, Epi::SwiGLU, hin, d, L.w_gu, d, uout, ff, M, 2 * ff, d, stream));
+        } else {
+            SURR_PHASE_RUN(ph_gu, surr::launch_gemm(a, Epi::StoreF32, hin, d, L.w_gu, d, gtmp, 2 * ff, M, 2 * ff, d, stream));
+            SURR_PHASE_RUN(ph_gu, surr::launch_swiglu_f32(gtmp, static_cast<float*>(uout), M, ff, stream));
+        }
+        SURR_PHASE_RUN(ph_down, surr::launch_gemm(a, Epi::ResidAddF32, uout, ff, L.w_down, ff, xres, d, M, d, ff, stream));
+        return SURR_OK;
+    };
+
+    SURR_PHASE_RUN(SURR_PHASE_EMBED, surr::launch_embed(a, tokens_d, row_stride, d_cu, batch, T, m->embed, d, c.vocab, x, d_pos, io.prefix ? d_pfx_len : nullptr, d_vt_off, d_vcol, m->err_flag, stream));
+    if (bf16)  // the projection epilogues never write these columns
+        SURR_PHASE_RUN(SURR_PHASE_EMBED, surr::launch_vt_pad_zero(vt, w.ld_vt, nkv * hd, d_cu, d_vt_off, batch, stream));
+    for (int l = 0; l < c.n_layers; ++l) {
+        const LayerW& L = m->layers[l];
+        const bool final_layer = l == c.n_layers - 1;
+        surr::PrefixKV pk;
+        if (io.prefix) {
+            pk.k = io.prefix->k(l);
+            pk.ld_k = m->d_kv();
+            pk.v = io.prefix->v(l);
+            pk.ld_v = bf16 ? io.prefix->rows : m->d_kv();
+            pk.len = d_pfx_len;
+            pk.off = d_pfx_off;
+        }
+        const surr::PrefixKV* pkp = io.prefix ? &pk : nullptr;
+        SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x, d, nullptr, T, L.attn_norm, d, c.rms_eps, h, d, stream));
+        if (a == Act::BF16) {
+            // RoPE on the q and k heads happens in the GEMM epilogue (one rounding)
+            surr::RopeArgs rope;
+            rope.pos = d_pos;
+            rope.cs = m->rope_cs;
+            rope.cols = (nq + nkv) * hd;
+            rope.head_dim = hd;
+            rope.vt = vt;
+            rope.ld_vt = w.ld_vt;
+            rope.vcol = d_vcol;
+            SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream, rope));
+        } else {
+            SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreAct, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream));
+            SURR_PHASE_RUN(SURR_PHASE_ROPE, surr::launch_rope(a, qkv, dqkv, T, d_pos, nq + nkv, hd, m->rope_cs, stream));
+        }
+        if (io.build) {
+            // keep this layer's keys and values for the prompts that will continue them
+            surrogate_prefix_cache* pc = io.capture;
+            SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, surr::launch_capture_rows(qkv, dqkv, dq, (int)m->d_kv(), (int)m->esz, d_cu, d_po, batch, pc->rows, pc->k(l), m->d_kv(), stream));
+            if (bf16)
+                SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, hipMemcpy2DAsync(pc->v(l), 2 * pc->rows, vt, 2 * w.ld_vt, 2 * pc->rows, m->d_kv(), hipMemcpyDeviceToDevice, stream));
+            else
+                SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, surr::launch_capture_rows(qkv, dqkv, dq + (int)m->d_kv(), (int)m->d_kv(), 4, d_cu, d_po, batch, pc->rows, pc->v(l), m->d_kv(), stream));
+            if (final_layer) break;  // nothing past the last layer's K/V is needed
+        }
+        if (!final_layer) {
+            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, vt, w.ld_vt, d_vt_off, o, dq, d_cu, d_work, (int)work.size(), nq, nkv, hd, stream, pkp));
+            SURR_PHASE_RUN(SURR_PHASE_GEMM_O, surr::launch_gemm(a, Epi::ResidAddF32, o, dq, L.w_o, dq, x, d, Ti, d, dq, stream));
+            SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x, d, nullptr, T, L.mlp_norm, d, c.rms_eps, h, d, stream));
+            const surrogate_status st = mlp(L, h, u, gu, x, Ti, SURR_PHASE_GEMM_GATE_UP, SURR_PHASE_GEMM_DOWN);
+            if (st != SURR_OK) return st;
+        } else {
+            // Only the last position of each prompt feeds the LM head: K/V above cover
+            // every token; attention, O projection and MLP run for the last rows only.
+            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, vt, w.ld_vt, d_vt_off, o, dq, d_cu, d_work_last, batch, nq, nkv, hd, stream, pkp));
+            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gather_rows(o, dq, d_last, batch, dq, (int)m->esz, o_last, dq, stream));
+            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gather_rows(x, d, d_last, batch, d, 4, x_last, d, stream));
+            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gemm(a, Epi::ResidAddF32, o_last, dq, L.w_o, dq, x_last, d, batch, d, dq, stream));
+            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, L.mlp_norm, d, c.rms_eps, h_last, d, stream));
+            const surrogate_status st = mlp(L, h_last, u_last, gu_last, x_last, batch, SURR_PHASE_LAST_ROWS, SURR_PHASE_LAST_ROWS);
+            if (st != SURR_OK) return st;
+        }
+    }
+    if (io.build) return SURR_OK;
+    SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, m->final_norm, d, c.rms_eps, y, d, stream));
+    SURR_PHASE_RUN(SURR_PHASE_LM_HEAD, surr::launch_gemm(a, Epi::StoreF32, y, d, m->lm_head, d, logits, c.vocab, batch, c.vocab, d, stream));
+    SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_verdict(logits, c.vocab, batch, c.vocab, d_vid, n_verdict, logprobs_d, probs_d, confidence_d, verdict_d, stream));
+#undef SURR_PHASE_RUN
+    return SURR_OK;
 }
 
 }  // namespace
@@ -321,188 +593,106 @@ surrogate_status surrogate_score_pairs(surrogate_model* m, const int32_t* tokens
     if (!m || !tokens_d || !lengths_h || !verdict_ids_h || !workspace_d || !logprobs_d ||
         !confidence_d)
         return fail(SURR_E_INVALID_ARG, "null argument");
-    const surrogate_config& c = m->cfg;
     if (batch < 1) return fail(SURR_E_INVALID_ARG, "batch must be >= 1");
-    if (n_verdict < 1 || n_verdict > 16) return fail(SURR_E_INVALID_ARG, "n_verdict must be in [1, 16]");
-    for (int i = 0; i < n_verdict; ++i) {
-        if (verdict_ids_h[i] < 0 || verdict_ids_h[i] >= c.vocab)
-            return fail(SURR_E_INVALID_ARG, "verdict id out of range");
-        for (int j = 0; j < i; ++j)
-            if (verdict_ids_h[j] == verdict_ids_h[i]) return fail(SURR_E_INVALID_ARG, "duplicate verdict id");
-    }
-    if (row_stride < 1) return fail(SURR_E_INVALID_ARG, "row_stride must be >= 1");
-    const int64_t cap = std::min<int64_t>(row_stride, c.max_pos);
-    int64_t T = 0;
-    for (int b = 0; b < batch; ++b) {
-        if (lengths_h[b] < 1 || lengths_h[b] > cap)
-            return fail(SURR_E_SHAPE, "length of prompt " + std::to_string(b) + " outside [1, min(row_stride, max_pos)]");
-        T += lengths_h[b];
-    }
-    if (T + 64 * (int64_t)batch > INT32_MAX)
-        return fail(SURR_E_SHAPE, "total tokens plus 64 per prompt exceed 2^31 - 1");
-    if (reinterpret_cast<uintptr_t>(workspace_d) % kAlign) return fail(SURR_E_INVALID_ARG, "workspace must be 256-byte aligned");
-    const WsLayout w = layout(m, batch, T);
-    if (workspace_bytes < w.total)
-        return fail(SURR_E_WORKSPACE, "workspace needs " + std::to_string(w.total) + " bytes");
+    const surrogate_status vs = check_verdicts(m->cfg, verdict_ids_h, n_verdict);
+    if (vs != SURR_OK) return vs;
+    PassIO io;
+    io.verdict_ids_h = verdict_ids_h;
+    io.n_verdict = n_verdict;
+    io.logprobs_d = logprobs_d;
+    io.probs_d = probs_d;
+    io.confidence_d = confidence_d;
+    io.verdict_d = verdict_d;
+    return run_pass(m, tokens_d, row_stride, lengths_h, batch, workspace_d, workspace_bytes, io, stream);
+}
 
-    // ---- plan: prompt offsets, last rows, verdict ids, attention work lists
-    const int qt = surr::attention_q_tile(m->act);
-    std::vector<int32_t> cu(batch + 1, 0), last(batch);
-    for (int b = 0; b < batch; ++b) {
-        cu[b + 1] = cu[b] + lengths_h[b];
-        last[b] = cu[b + 1] - 1;
+surrogate_status surrogate_prefix_build(surrogate_model* m, const int32_t* tokens_d,
+                                        int64_t row_stride, const int32_t* lengths_h,
+                                        int32_t n_prefix, void* workspace_d,
+                                        size_t workspace_bytes, hipStream_t stream,
+                                        surrogate_prefix_cache** out) {
+    if (!m || !tokens_d || !lengths_h || !workspace_d || !out) return fail(SURR_E_INVALID_ARG, "null argument");
+    *out = nullptr;
+    if (n_prefix < 1) return fail(SURR_E_INVALID_ARG, "n_prefix must be >= 1");
+    auto* pc = new surrogate_prefix_cache();
+    pc->model = m;
+    pc->len.assign(lengths_h, lengths_h + n_prefix);
+    pc->off.resize(n_prefix);
+    for (int g = 0; g < n_prefix; ++g) {
+        pc->off[g] = (int32_t)pc->rows;
+        pc->rows += (std::max(lengths_h[g], 0) + 63) / 64 * 64;
     }
-    std::vector<int32_t> vt_off(batch + 1, 0);
-    for (int b = 0; b < batch; ++b) vt_off[b + 1] = vt_off[b] + (lengths_h[b] + 63) / 64 * 64;
-    std::vector<int2> work, work_last(batch);
-    for (int b = 0; b < batch; ++b) {
-        for (int t = 0; t * qt < lengths_h[b]; ++t) work.push_back(make_int2(b, t));
-        work_last[b] = make_int2(b, (lengths_h[b] - 1) / qt);
+    // 32-bit DMA offsets over one kv head's V^T rows of the cache
+    if (pc->rows * m->cfg.head_dim * 2 > (int64_t)UINT32_MAX || pc->rows > INT32_MAX) {
+        delete pc;
+        return fail(SURR_E_SHAPE, "prefixes too long for one cache");
     }
-    // Longest key range first, so the big causal tiles start early; stable for
-    // a deterministic order.
-    auto kv_len = [&](const int2& it) { return std::min(lengths_h[it.x], (it.y + 1) * qt); };
-    std::stable_sort(work.begin(), work.end(),
-                     [&](const int2& a, const int2& b) { return kv_len(a) > kv_len(b); });
-
-    const size_t meta_bytes = w.pos;  // cu .. vt_off are contiguous from offset 0
-    {
-        std::lock_guard<std::mutex> lock(m->mu);
-        if (m->staged_pending) SURR_HIP(hipEventSynchronize(m->staged));
-        m->staged_pending = false;
-        if (m->pinned_bytes < meta_bytes) {
-            if (m->pinned) SURR_HIP(hipHostFree(m->pinned));
-            m->pinned = nullptr;
-            m->pinned_bytes = 0;
-            if (hipHostMalloc(&m->pinned, meta_bytes, hipHostMallocDefault) != hipSuccess)
-                return fail(SURR_E_OOM, "pinned staging buffer");
-            m->pinned_bytes = meta_bytes;
+    pc->k_bytes = align_up((size_t)pc->rows * m->d_kv() * m->esz);
+    pc->v_bytes = pc->k_bytes;
+    const size_t bytes = (size_t)m->cfg.n_layers * (pc->k_bytes + pc->v_bytes);
+    PassIO io;
+    io.build = true;
+    io.capture = pc;
+    // arguments are checked before the cache memory is taken
+    surrogate_status st = SURR_OK;
+    for (int g = 0; g < n_prefix && st == SURR_OK; ++g)
+        if (lengths_h[g] < 1 || lengths_h[g] > std::min<int64_t>(row_stride, m->cfg.max_pos - 1))
+            st = fail(SURR_E_SHAPE, "length of prefix " + std::to_string(g) + " outside [1, min(row_stride, max_pos - 1)]");
+    if (st == SURR_OK && hipMalloc(&pc->mem, bytes) != hipSuccess) {
+        pc->mem = nullptr;
+        st = fail(SURR_E_OOM, "prefix cache of " + std::to_string(bytes) + " bytes");
+    }
+    if (st == SURR_OK)
+        st = run_pass(m, tokens_d, row_stride, lengths_h, n_prefix, workspace_d, workspace_bytes, io, stream);
+    if (st != SURR_OK) {
+        if (pc->mem) {
+            hipStreamSynchronize(stream);
+            hipFree(pc->mem);
         }
-        char* P = static_cast<char*>(m->pinned);
-        std::memcpy(P + w.cu, cu.data(), 4 * cu.size());
-        std::memcpy(P + w.last, last.data(), 4 * last.size());
-        std::memcpy(P + w.vid, verdict_ids_h, 4 * (size_t)n_verdict);
-        std::memcpy(P + w.work, work.data(), 8 * work.size());
-        std::memcpy(P + w.work_last, work_last.data(), 8 * work_last.size());
-        std::memcpy(P + w.vt_off, vt_off.data(), 4 * vt_off.size());
-        SURR_HIP(hipMemcpyAsync(workspace_d, P, meta_bytes, hipMemcpyHostToDevice, stream));
-        SURR_HIP(hipEventRecord(m->staged, stream));
-        m->staged_pending = true;
+        delete pc;
+        return st;
     }
-
-    char* W = static_cast<char*>(workspace_d);
-    const int32_t* d_cu = reinterpret_cast<const int32_t*>(W + w.cu);
-    const int32_t* d_last = reinterpret_cast<const int32_t*>(W + w.last);
-    const int32_t* d_vid = reinterpret_cast<const int32_t*>(W + w.vid);
-    const int2* d_work = reinterpret_cast<const int2*>(W + w.work);
-    const int2* d_work_last = reinterpret_cast<const int2*>(W + w.work_last);
-    int32_t* d_pos = reinterpret_cast<int32_t*>(W + w.pos);
-    const bool bf16 = m->act == Act::BF16;
-    const int32_t* d_vt_off = bf16 ? reinterpret_cast<const int32_t*>(W + w.vt_off) : nullptr;
-    int32_t* d_vcol = bf16 ? reinterpret_cast<int32_t*>(W + w.vcol) : nullptr;
-    uint16_t* vt = bf16 ? reinterpret_cast<uint16_t*>(W + w.vt) : nullptr;
-    float* x = reinterpret_cast<float*>(W + w.x);
-    void* h = W + w.h;
-    void* qkv = W + w.qkv;
-    void* o = W + w.o;
-    void* u = W + w.u;
-    float* gu = reinterpret_cast<float*>(W + w.gu);
-    void* o_last = W + w.o_last;
-    float* x_last = reinterpret_cast<float*>(W + w.x_last);
-    void* h_last = W + w.h_last;
-    void* u_last = W + w.u_last;
-    float* gu_last = reinterpret_cast<float*>(W + w.gu_last);
-    void* y = W + w.y;
-    float* logits = reinterpret_cast<float*>(W + w.logits);
-
-    const Act a = m->act;
-    const int d = c.d_model, ff = c.d_ff, nq = c.n_q_heads, nkv = c.n_kv_heads, hd = c.head_dim;
-    const int dq = (int)m->d_q(), dqkv = (int)m->d_qkv();
-    const int Ti = (int)T;
-
-
-    // Phase bracketing for the measurement hook (a no-op unless profiling is on).
-    auto mark = [&](int phase) -> hipError_t {
-        if (!m->profiling) return hipSuccess;
-        while (m->ev_used + 2 > m->ev_pool.size()) {
-            hipEvent_t e;
-            hipError_t r = hipEventCreate(&e);
-            if (r != hipSuccess) return r;
-            m->ev_pool.push_back(e);
-        }
-        m->rec.emplace_back(phase, m->ev_used);
-        const hipEvent_t e0 = m->ev_pool[m->ev_used];
-        m->ev_used += 2;
-        return hipEventRecord(e0, stream);
-    };
-    auto done = [&]() -> hipError_t {
-        if (!m->profiling) return hipSuccess;
-        return hipEventRecord(m->ev_pool[m->rec.back().second + 1], stream);
-    };
-#define SURR_PHASE_RUN(phase, expr)  \
-    do {                             \
-        SURR_HIP(mark(phase));       \
-        SURR_HIP(expr);              \
-        SURR_HIP(done());            \
-    } while (0)
-
-    auto mlp = [&](const LayerW& L, void* hin, void* uout, float* gtmp, float* xres, int M,
-                   int ph_gu, int ph_down) -> surrogate_status {
-        if (a == Act::BF16) {
-            SURR_PHASE_RUN(ph_gu, surr::launch_gemm(a, Epi::SwiGLU, hin, d, L.w_gu, d, uout, ff, M, 2 * ff, d, stream));
-        } else {
-            SURR_PHASE_RUN(ph_gu, surr::launch_gemm(a, Epi::StoreF32, hin, d, L.w_gu, d, gtmp, 2 * ff, M, 2 * ff, d, stream));
-            SURR_PHASE_RUN(ph_gu, surr::launch_swiglu_f32(gtmp, static_cast<float*>(uout), M, ff, stream));
-        }
-        SURR_PHASE_RUN(ph_down, surr::launch_gemm(a, Epi::ResidAddF32, uout, ff, L.w_down, ff, xres, d, M, d, ff, stream));
-        return SURR_OK;
-    };
-
-    SURR_PHASE_RUN(SURR_PHASE_EMBED, surr::launch_embed(a, tokens_d, row_stride, d_cu, batch, T, m->embed, d, c.vocab, x, d_pos, d_vt_off, d_vcol, m->err_flag, stream));
-    if (bf16)  // the projection epilogues never write these columns
-        SURR_PHASE_RUN(SURR_PHASE_EMBED, surr::launch_vt_pad_zero(vt, w.ld_vt, nkv * hd, d_cu, d_vt_off, batch, stream));
-    for (int l = 0; l < c.n_layers; ++l) {
-        const LayerW& L = m->layers[l];
-        const bool final_layer = l == c.n_layers - 1;
-        SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x, d, nullptr, T, L.attn_norm, d, c.rms_eps, h, d, stream));
-        if (a == Act::BF16) {
-            // RoPE on the q and k heads happens in the GEMM epilogue (one rounding)
-            surr::RopeArgs rope;
-            rope.pos = d_pos;
-            rope.cs = m->rope_cs;
-            rope.cols = (nq + nkv) * hd;
-            rope.head_dim = hd;
-            rope.vt = vt;
-            rope.ld_vt = w.ld_vt;
-            rope.vcol = d_vcol;
-            SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream, rope));
-        } else {
-            SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreAct, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream));
-            SURR_PHASE_RUN(SURR_PHASE_ROPE, surr::launch_rope(a, qkv, dqkv, T, d_pos, nq + nkv, hd, m->rope_cs, stream));
-        }
-        if (!final_layer) {
-            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, vt, w.ld_vt, d_vt_off, o, dq, d_cu, d_work, (int)work.size(), nq, nkv, hd, stream));
-            SURR_PHASE_RUN(SURR_PHASE_GEMM_O, surr::launch_gemm(a, Epi::ResidAddF32, o, dq, L.w_o, dq, x, d, Ti, d, dq, stream));
-            SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x, d, nullptr, T, L.mlp_norm, d, c.rms_eps, h, d, stream));
-            const surrogate_status st = mlp(L, h, u, gu, x, Ti, SURR_PHASE_GEMM_GATE_UP, SURR_PHASE_GEMM_DOWN);
-            if (st != SURR_OK) return st;
-        } else {
-            // Only the last position of each prompt feeds the LM head: K/V above cover
-            // every token; attention, O projection and MLP run for the last rows only.
-            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, vt, w.ld_vt, d_vt_off, o, dq, d_cu, d_work_last, batch, nq, nkv, hd, stream));
-            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gather_rows(o, dq, d_last, batch, dq, (int)m->esz, o_last, dq, stream));
-            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gather_rows(x, d, d_last, batch, d, 4, x_last, d, stream));
-            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gemm(a, Epi::ResidAddF32, o_last, dq, L.w_o, dq, x_last, d, batch, d, dq, stream));
-            SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, L.mlp_norm, d, c.rms_eps, h_last, d, stream));
-            const surrogate_status st = mlp(L, h_last, u_last, gu_last, x_last, batch, SURR_PHASE_LAST_ROWS, SURR_PHASE_LAST_ROWS);
-            if (st != SURR_OK) return st;
-        }
-    }
-    SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, m->final_norm, d, c.rms_eps, y, d, stream));
-    SURR_PHASE_RUN(SURR_PHASE_LM_HEAD, surr::launch_gemm(a, Epi::StoreF32, y, d, m->lm_head, d, logits, c.vocab, batch, c.vocab, d, stream));
-    SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_verdict(logits, c.vocab, batch, c.vocab, d_vid, n_verdict, logprobs_d, probs_d, confidence_d, verdict_d, stream));
-#undef SURR_PHASE_RUN
+    *out = pc;
     return SURR_OK;
+}
+
+surrogate_status surrogate_score_suffixes(surrogate_model* m, const surrogate_prefix_cache* cache,
+                                          const int32_t* prefix_id_h, const int32_t* tokens_d,
+                                          int64_t row_stride, const int32_t* lengths_h,
+                                          int32_t batch, const int32_t* verdict_ids_h,
+                                          int32_t n_verdict, void* workspace_d,
+                                          size_t workspace_bytes, float* logprobs_d,
+                                          float* probs_d, float* confidence_d, int32_t* verdict_d,
+                                          hipStream_t stream) {
+    if (!m || !cache || !prefix_id_h || !tokens_d || !lengths_h || !verdict_ids_h ||
+        !workspace_d || !logprobs_d || !confidence_d)
+        return fail(SURR_E_INVALID_ARG, "null argument");
+    if (cache->model != m) return fail(SURR_E_INVALID_ARG, "prefix cache was built by another model");
+    if (batch < 1) return fail(SURR_E_INVALID_ARG, "batch must be >= 1");
+    const surrogate_status vs = check_verdicts(m->cfg, verdict_ids_h, n_verdict);
+    if (vs != SURR_OK) return vs;
+    PassIO io;
+    io.prefix = cache;
+    io.prefix_id_h = prefix_id_h;
+    io.verdict_ids_h = verdict_ids_h;
+    io.n_verdict = n_verdict;
+    io.logprobs_d = logprobs_d;
+    io.probs_d = probs_d;
+    io.confidence_d = confidence_d;
+    io.verdict_d = verdict_d;
+    return run_pass(m, tokens_d, row_stride, lengths_h, batch, workspace_d, workspace_bytes, io, stream);
+}
+
+surrogate_status surrogate_prefix_cache_bytes(const surrogate_prefix_cache* cache, size_t* bytes) {
+    if (!cache || !bytes) return fail(SURR_E_INVALID_ARG, "null argument");
+    *bytes = (size_t)cache->model->cfg.n_layers * (cache->k_bytes + cache->v_bytes);
+    return SURR_OK;
+}
+
+void surrogate_prefix_free(surrogate_prefix_cache* cache) {
+    if (!cache) return;
+    if (cache->mem) hipFree(cache->mem);
+    delete cache;
 }
 
 surrogate_status surrogate_select(const float* confidence_d, int32_t n, surrogate_select_mode mode,

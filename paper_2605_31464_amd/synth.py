@@ -220,3 +220,68 @@ def bin_forecasts(n: int, n_bins: int = 8, seed: int = 2) -> np.ndarray:
     g = rng.gamma(alpha[:, None], 1.0, size=(n, n_bins))
     g = np.maximum(g, 1e-30)
     return (g / g.sum(axis=1, keepdims=True)).astype(np.float32)
+
+
+@dataclasses.dataclass(frozen=True)
+class PrefixWorkload:
+    """Candidates that share per-task prompt prefixes (the system prompt plus the task's
+    reference kernel), each followed by its own candidate suffix."""
+    name: str
+    shape: ModelShape
+    n_tasks: int
+    batch: int
+    prefix_lengths: tuple  # ("lognormal", median, sigma, lo, hi) or ("uniform", lo, hi)
+    suffix_lengths: tuple
+    n_verdict: int
+
+
+PREFIX_CONFIGS = {
+    "7b-prefix": PrefixWorkload("7B-bf16-shared-prefix", CONFIGS["7b"].shape, 6, 128,
+                                ("lognormal", 2048, 0.5, 1024, 4096),
+                                ("lognormal", 1024, 0.5, 256, 4096), 2),
+}
+
+
+def _draw(spec, n, rng):
+    if spec[0] == "uniform":
+        return rng.integers(spec[1], spec[2] + 1, size=n).astype(np.int32)
+    _, median, sigma, lo, hi = spec
+    return np.clip(np.rint(np.exp(rng.normal(math.log(median), sigma, size=n))), lo, hi).astype(np.int32)
+
+
+def make_prefix_prompts(w: PrefixWorkload, seed: int = 1):
+    """(prefix tokens [G, Pmax], prefix lengths [G], suffix tokens [B, Smax], suffix lengths
+    [B], prefix id of each candidate [B]).  ``default_rng(seed)`` draws the prefix lengths,
+    the suffix lengths, then all prefix tokens and all suffix tokens back to back (Zipf(1.1)
+    ranks as in make_prompts); candidate i belongs to task i mod G."""
+    rng = np.random.default_rng(seed)
+    V = w.shape.vocab
+    Lp = _draw(w.prefix_lengths, w.n_tasks, rng)
+    Ls = _draw(w.suffix_lengths, w.batch, rng)
+    cdf = zipf_cdf(V)
+
+    def tokens(L):
+        ids = np.minimum(np.searchsorted(cdf, rng.random(int(L.sum())), side="right"), V - 1)
+        tok = np.zeros((len(L), int(L.max())), np.int32)
+        off = 0
+        for b, n in enumerate(L):
+            tok[b, :n] = ids[off:off + n]
+            off += n
+        return tok
+
+    ptok = tokens(Lp)
+    stok = tokens(Ls)
+    pid = (np.arange(w.batch) % w.n_tasks).astype(np.int32)
+    return ptok, Lp, stok, Ls, pid
+
+
+def concat_prompts(ptok, Lp, stok, Ls, pid):
+    """Padded [B, max(Lp[pid] + Ls)] matrix of the full prompts prefix ++ suffix (-1: none)."""
+    full_len = np.array([(Lp[g] if g >= 0 else 0) + n for g, n in zip(pid, Ls)], np.int32)
+    tok = np.zeros((len(Ls), int(full_len.max())), np.int32)
+    for i, (g, n) in enumerate(zip(pid, Ls)):
+        p = int(Lp[g]) if g >= 0 else 0
+        if p:
+            tok[i, :p] = ptok[g, :p]
+        tok[i, p:p + n] = stok[i, :n]
+    return tok, full_len

@@ -23,7 +23,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = B.lib()
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 18
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B.EXPORTS)
@@ -107,6 +107,23 @@ def test_forecast_head_rejects_bad_arguments_synchronously():
     assert call(m_=bad_m.ctypes.data) == B.SURR_E_INVALID_ARG
     assert call(nb=1, cut=(1.0,)) == B.SURR_E_INVALID_ARG
     assert b"cutoff" in L.surrogate_last_error() or L.surrogate_last_error()
+
+
+def test_prefix_calls_reject_bad_arguments_synchronously():
+    L = B.lib()
+    p = ctypes.c_void_p(256)
+    lens = np.array([3], np.int32)
+    pid = np.array([0], np.int32)
+    vid = np.array([1], np.int32)
+    h = ctypes.c_void_p()
+    assert L.surrogate_prefix_build(None, p, 4, lens.ctypes.data, 1, p, 1 << 20, None,
+                                    ctypes.byref(h)) == B.SURR_E_INVALID_ARG and not h.value
+    assert L.surrogate_score_suffixes(None, p, pid.ctypes.data, p, 4, lens.ctypes.data, 1,
+                                      vid.ctypes.data, 1, p, 1 << 20, p, None, p, None,
+                                      None) == B.SURR_E_INVALID_ARG
+    n = ctypes.c_size_t()
+    assert L.surrogate_prefix_cache_bytes(None, ctypes.byref(n)) == B.SURR_E_INVALID_ARG
+    L.surrogate_prefix_free(None)  # ignored
 
 
 def test_score_pairs_rejects_null_model():
