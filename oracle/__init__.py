@@ -18,11 +18,14 @@ definition:
 * ``forecast``    - the paper's eight-bin speedup head: expected speedup
   S_hat = sum_b p_b m_b (Section 3.1, Table 3), discovery score Pr[g >= x]
   (Section 3.6) and the top-k candidates by S_hat (Sections 3.1 and 3.5).
+* ``evaluate``    - forecast quality against measured speedups: measured bins, the
+  correctness, Brier and CRPS rewards (Section 2.2), ECE, forecast error and speedup
+  recovered (Section 3.1).
 
 Parity status: every function is pinned by ``tests/test_oracle_pins.py`` and
-``tests/test_oracle_forecast_pins.py`` (closed
+``tests/test_oracle_forecast_pins.py`` and ``tests/test_oracle_evaluate_pins.py`` (closed
 forms, invariants, a hand-computed one-layer case, independent library routines,
 brute force).  The absolute bf16 error at full depth has no closed form; it is
 bounded only by comparison with this oracle at the stated tolerances.
 """
-from . import forecast, select, transformer  # noqa: F401
+from . import evaluate, forecast, select, transformer  # noqa: F401
