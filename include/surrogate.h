@@ -220,6 +220,34 @@ surrogate_status surrogate_forecast_head(const float *probs_d, int64_t n, int32_
                                          float *expected_speedup_d, float *discovery_d,
                                          hipStream_t stream);
 
+/* Forecast quality against measured speedups, for batches of evaluation candidates or RL
+ * rollouts.  probs_d [n, n_bins] are forecasts (device, row-major), speedup_d [n] the
+ * measured speedups S_i = T_ref / T_i (device, finite and positive), 1 <= n <= 65536,
+ * 2 <= n_bins <= 16; bin_values_h / bin_edges_h as in surrogate_forecast_head (bin b
+ * covers (edge[b-1], edge[b]]; a speedup's bin counts the edges strictly below it).
+ * budgets_h [n_budgets], 1 <= n_budgets <= 8, are fractions c in (0, 1]: the top
+ * max(1, floor(c n)) candidates by expected speedup are measured (ties by index).
+ * Outputs (device; the per-candidate ones may be NULL):
+ *  bin_d     int32 [n]: the measured bin y_i.
+ *  brier_d   float [n]: Brier(p_i, y_i) = 1/2 sum_b (p_{i,b} - 1[b = y_i])^2 (Section 2.2).
+ *  crps_d    float [n]: CRPS = 1/(n_bins - 1) sum_{k < n_bins - 1} (F_k - 1[y_i <= k])^2.
+ *  summary_d double [8 + n_budgets]: accuracy (mean of the correctness reward
+ *            1[argmax p_i = y_i], first argmax), mean Brier, mean CRPS, mean
+ *            r_corr + 1 - Brier, mean r_corr + 1 - CRPS (Section 2.2), ECE over ten
+ *            confidence buckets (floor(10 q) in float32, q = 1 in the last), forecast
+ *            error mean |m_{argmax} - S_i|, speedup recovered averaged over the budgets
+ *            (percent), then speedup recovered at each budget (Section 3.1).
+ * workspace_d: device, 256-byte aligned, >= surrogate_evaluate_workspace_size(n, n_budgets).
+ * Sums are taken in float64 in a fixed order (deterministic).
+ * Errors (synchronous): SURR_E_INVALID_ARG, SURR_E_WORKSPACE, SURR_E_HIP. */
+surrogate_status surrogate_evaluate_workspace_size(int32_t n, int32_t n_budgets, size_t *bytes);
+surrogate_status surrogate_evaluate(const float *probs_d, const float *speedup_d, int32_t n,
+                                    int32_t n_bins, const double *bin_values_h,
+                                    const double *bin_edges_h, const double *budgets_h,
+                                    int32_t n_budgets, void *workspace_d, size_t workspace_bytes,
+                                    int32_t *bin_d, float *brier_d, float *crps_d,
+                                    double *summary_d, hipStream_t stream);
+
 /* Synchronize `stream` and report (then clear) the sticky device error of the model:
  * SURR_E_TOKEN_RANGE if an out-of-range token id was seen since the last check. */
 surrogate_status surrogate_device_status(surrogate_model *m, hipStream_t stream);

@@ -29,7 +29,8 @@ EXPORTS = ("surrogate_tensor_count", "surrogate_tensor_shape", "surrogate_load_w
            "surrogate_select", "surrogate_device_status", "surrogate_free",
            "surrogate_status_string", "surrogate_last_error", "surrogate_profile_enable",
            "surrogate_profile_collect", "surrogate_forecast_head", "surrogate_prefix_build",
-           "surrogate_score_suffixes", "surrogate_prefix_cache_bytes", "surrogate_prefix_free")
+           "surrogate_score_suffixes", "surrogate_prefix_cache_bytes", "surrogate_prefix_free",
+           "surrogate_evaluate_workspace_size", "surrogate_evaluate")
 PHASES = ("embed", "rmsnorm", "gemm_qkv", "rope", "attention", "gemm_o", "gemm_gate_up",
           "gemm_down", "last_rows", "lm_head", "lse_verdict", "prefix_capture")
 
@@ -81,6 +82,8 @@ def lib() -> ctypes.CDLL:
         "surrogate_score_suffixes": (I32, [P, P, P, P, I64, P, I32, P, I32, P, SZ, P, P, P, P, P]),
         "surrogate_prefix_cache_bytes": (I32, [P, ctypes.POINTER(SZ)]),
         "surrogate_prefix_free": (None, [P]),
+        "surrogate_evaluate_workspace_size": (I32, [I32, I32, ctypes.POINTER(SZ)]),
+        "surrogate_evaluate": (I32, [P, P, I32, I32, P, P, P, I32, P, SZ, P, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -305,6 +308,48 @@ def surrogate_forecast_head(probs, bin_values, bin_edges=None, cutoffs=(), expec
         ptr(probs), n, nb, host(m), host(e), host(cut), nc, ptr(expected_speedup),
         ptr(discovery if nc else None), ctypes.c_void_p(_stream(stream))), "surrogate_forecast_head")
     return expected_speedup, (discovery if nc else None)
+
+
+SUMMARY_FIELDS = ("accuracy", "brier", "crps", "reward_brier", "reward_crps", "ece",
+                  "forecast_error", "recovered")
+
+
+def surrogate_evaluate_workspace_size(n: int, n_budgets: int) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().surrogate_evaluate_workspace_size(n, n_budgets, ctypes.byref(out)),
+           "surrogate_evaluate_workspace_size")
+    return out.value
+
+
+def surrogate_evaluate(probs, speedup, bin_values, bin_edges, budgets=(0.01, 0.05, 0.10, 0.25, 0.50),
+                       per_candidate=True, workspace=None, stream=None):
+    """probs: float32 device [n, n_bins]; speedup: float32 device [n].  Returns (summary
+    float64 device tensor [8 + n_budgets], bins, brier, crps) with the per-candidate
+    tensors None unless per_candidate."""
+    import torch
+    if probs.dtype != torch.float32 or probs.dim() != 2 or not probs.is_contiguous():
+        raise ValueError("probs must be a contiguous float32 [n, n_bins] device tensor")
+    if speedup.dtype != torch.float32 or speedup.numel() != probs.shape[0]:
+        raise ValueError("speedup must be float32 with one entry per forecast")
+    n, nb = int(probs.shape[0]), int(probs.shape[1])
+    m = np.ascontiguousarray(np.asarray(bin_values, np.float64))
+    e = np.ascontiguousarray(np.asarray(bin_edges, np.float64))
+    c = np.ascontiguousarray(np.asarray(budgets, np.float64))
+    dev = probs.device
+    if workspace is None:
+        workspace = torch.empty(surrogate_evaluate_workspace_size(n, int(c.size)),
+                                dtype=torch.uint8, device=dev)
+    summary = torch.empty(8 + c.size, dtype=torch.float64, device=dev)
+    bins = torch.empty(n, dtype=torch.int32, device=dev) if per_candidate else None
+    br = torch.empty(n, dtype=torch.float32, device=dev) if per_candidate else None
+    cr = torch.empty(n, dtype=torch.float32, device=dev) if per_candidate else None
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
+    _check(lib().surrogate_evaluate(
+        ptr(probs), ptr(speedup), n, nb, m.ctypes.data_as(ctypes.c_void_p),
+        e.ctypes.data_as(ctypes.c_void_p), c.ctypes.data_as(ctypes.c_void_p), int(c.size),
+        ptr(workspace), workspace.numel() * workspace.element_size(), ptr(bins), ptr(br), ptr(cr),
+        ptr(summary), ctypes.c_void_p(_stream(stream))), "surrogate_evaluate")
+    return summary, bins, br, cr
 
 
 def surrogate_device_status(model: Model, stream=None) -> int:

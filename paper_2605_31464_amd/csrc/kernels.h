@@ -75,6 +75,28 @@ struct BinWeights {
 hipError_t launch_forecast_head(const float* probs, int64_t n, int n_bins, const BinWeights& w,
                                 int n_cutoffs, float* speedup, float* disc, hipStream_t s);
 
+// ---- k_evaluate.hip
+// Bin edges (float64, compared against float32 speedups) and representatives of the
+// forecast bins.
+struct EvalBins {
+    double edge[kMaxBins - 1];
+    float value[kMaxBins];
+};
+
+// Per candidate: measured bin, Brier, CRPS (outputs optional), plus per-workgroup partial
+// sums in `partial` (eval_partial_bytes(n, n_budgets) bytes).  Then eval_finalize, after
+// the top-score selection of every budget into lists + 2 n c (counts[2 c] entries), writes
+// summary[0..6] = accuracy, mean Brier, mean CRPS, mean r_corr + 1 - Brier, mean
+// r_corr + 1 - CRPS, ECE (10 buckets), forecast error; summary[8 + c] = 100 * max speedup
+// over budget c's list / max speedup and summary[7] their mean.  2 <= n_bins <= 16.
+size_t eval_partial_bytes(int n, int n_budgets);
+hipError_t launch_eval_metrics(const float* probs, const float* speedup, int n, int n_bins,
+                               const EvalBins& bins, int32_t* bin_out, float* brier_out,
+                               float* crps_out, double* partial, hipStream_t s);
+hipError_t launch_eval_finalize(const float* speedup, int n, const int32_t* lists,
+                                const int32_t* counts, int n_budgets, double* partial,
+                                double* summary, hipStream_t s);
+
 // ---- k_gemm.hip
 enum class Epi { StoreAct, ResidAddF32, SwiGLU, StoreF32, StoreActRope };
 

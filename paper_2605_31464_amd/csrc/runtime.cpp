@@ -763,6 +763,64 @@ surrogate_status surrogate_forecast_head(const float* probs_d, int64_t n, int32_
     return SURR_OK;
 }
 
+surrogate_status surrogate_evaluate_workspace_size(int32_t n, int32_t n_budgets, size_t* bytes) {
+    if (!bytes) return fail(SURR_E_INVALID_ARG, "null argument");
+    if (n < 1 || n > 65536) return fail(SURR_E_INVALID_ARG, "n must be in [1, 65536]");
+    if (n_budgets < 1 || n_budgets > 8) return fail(SURR_E_INVALID_ARG, "n_budgets must be in [1, 8]");
+    // expected speedups, per budget the two index lists, the counts, the partial rows
+    *bytes = align_up(4 * (size_t)n) + align_up(8 * (size_t)n * n_budgets) +
+             align_up(8 * (size_t)n_budgets) + align_up(surr::eval_partial_bytes(n, n_budgets));
+    return SURR_OK;
+}
+
+surrogate_status surrogate_evaluate(const float* probs_d, const float* speedup_d, int32_t n,
+                                    int32_t n_bins, const double* bin_values_h,
+                                    const double* bin_edges_h, const double* budgets_h,
+                                    int32_t n_budgets, void* workspace_d, size_t workspace_bytes,
+                                    int32_t* bin_d, float* brier_d, float* crps_d,
+                                    double* summary_d, hipStream_t stream) {
+    if (!probs_d || !speedup_d || !bin_values_h || !bin_edges_h || !budgets_h || !workspace_d ||
+        !summary_d)
+        return fail(SURR_E_INVALID_ARG, "null argument");
+    if (n_bins < 2 || n_bins > surr::kMaxBins) return fail(SURR_E_INVALID_ARG, "n_bins must be in [2, 16]");
+    size_t need = 0;
+    const surrogate_status st = surrogate_evaluate_workspace_size(n, n_budgets, &need);
+    if (st != SURR_OK) return st;
+    if (workspace_bytes < need) return fail(SURR_E_WORKSPACE, "workspace needs " + std::to_string(need) + " bytes");
+    if (reinterpret_cast<uintptr_t>(workspace_d) % kAlign) return fail(SURR_E_INVALID_ARG, "workspace must be 256-byte aligned");
+    surr::EvalBins eb{};
+    surr::BinWeights hw{};
+    for (int b = 0; b < n_bins; ++b) {
+        if (!std::isfinite(bin_values_h[b])) return fail(SURR_E_INVALID_ARG, "non-finite bin value");
+        eb.value[b] = (float)bin_values_h[b];
+        hw.w[b][0] = (float)bin_values_h[b];
+    }
+    for (int j = 0; j < n_bins - 1; ++j) {
+        if (!std::isfinite(bin_edges_h[j]) || !(bin_edges_h[j] > 0.0) ||
+            (j > 0 && !(bin_edges_h[j] > bin_edges_h[j - 1])))
+            return fail(SURR_E_INVALID_ARG, "bin edges must be finite, positive, strictly increasing");
+        eb.edge[j] = bin_edges_h[j];
+    }
+    std::vector<int> ks(n_budgets);
+    for (int c = 0; c < n_budgets; ++c) {
+        if (!(budgets_h[c] > 0.0 && budgets_h[c] <= 1.0)) return fail(SURR_E_INVALID_ARG, "budgets must lie in (0, 1]");
+        ks[c] = std::max(1, (int)std::floor(budgets_h[c] * n));  // top c%, at least one
+    }
+    char* W = static_cast<char*>(workspace_d);
+    float* shat = reinterpret_cast<float*>(W);
+    int32_t* lists = reinterpret_cast<int32_t*>(W + align_up(4 * (size_t)n));
+    int32_t* counts = reinterpret_cast<int32_t*>(W + align_up(4 * (size_t)n) + align_up(8 * (size_t)n * n_budgets));
+    double* partial = reinterpret_cast<double*>(W + align_up(4 * (size_t)n) + align_up(8 * (size_t)n * n_budgets) + align_up(8 * (size_t)n_budgets));
+    SURR_HIP(surr::launch_eval_metrics(probs_d, speedup_d, n, n_bins, eb, bin_d, brier_d, crps_d, partial, stream));
+    SURR_HIP(surr::launch_forecast_head(probs_d, n, n_bins, hw, 0, shat, nullptr, stream));
+    for (int c = 0; c < n_budgets; ++c) {
+        int32_t* d = lists + (size_t)c * 2 * n;
+        SURR_HIP(surr::launch_select(shat, n, 2, 0.f, ks[c], d, d + n, counts + 2 * c, stream));
+    }
+    SURR_HIP(surr::launch_eval_finalize(speedup_d, n, lists, counts, n_budgets, partial, summary_d, stream));
+    return SURR_OK;
+}
+
 surrogate_status surrogate_device_status(surrogate_model* m, hipStream_t stream) {
     if (!m) return fail(SURR_E_INVALID_ARG, "null argument");
     int32_t flag = 0;

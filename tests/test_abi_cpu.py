@@ -23,7 +23,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = B.lib()
     names = declared_functions()
-    assert len(names) == 18
+    assert len(names) == 20
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B.EXPORTS)
@@ -124,6 +124,34 @@ def test_prefix_calls_reject_bad_arguments_synchronously():
     n = ctypes.c_size_t()
     assert L.surrogate_prefix_cache_bytes(None, ctypes.byref(n)) == B.SURR_E_INVALID_ARG
     L.surrogate_prefix_free(None)  # ignored
+
+
+def test_evaluate_rejects_bad_arguments_synchronously():
+    L = B.lib()
+    p = ctypes.c_void_p(256)
+    m = np.arange(1, 9, dtype=np.float64)
+    e = 2.0 ** np.array([-2, -1, -0.5, 0, 0.5, 1, 2])
+    c = np.array([0.25], np.float64)
+    sz = ctypes.c_size_t()
+    assert L.surrogate_evaluate_workspace_size(0, 1, ctypes.byref(sz)) == B.SURR_E_INVALID_ARG
+    assert L.surrogate_evaluate_workspace_size(65537, 1, ctypes.byref(sz)) == B.SURR_E_INVALID_ARG
+    assert L.surrogate_evaluate_workspace_size(10, 9, ctypes.byref(sz)) == B.SURR_E_INVALID_ARG
+    assert L.surrogate_evaluate_workspace_size(10, 5, ctypes.byref(sz)) == B.SURR_OK and sz.value
+
+    def call(n=10, nb=8, m_=m, e_=e, c_=c, ws_bytes=1 << 20):
+        return L.surrogate_evaluate(p, p, n, nb, m_.ctypes.data, e_.ctypes.data, c_.ctypes.data,
+                                    c_.size, p, ws_bytes, None, None, None, p, None)
+
+    assert call(nb=1) == B.SURR_E_INVALID_ARG
+    assert call(nb=17) == B.SURR_E_INVALID_ARG
+    assert call(ws_bytes=16) == B.SURR_E_WORKSPACE
+    assert call(c_=np.array([0.0])) == B.SURR_E_INVALID_ARG
+    assert call(c_=np.array([1.5])) == B.SURR_E_INVALID_ARG
+    bad = e.copy()
+    bad[2] = -1.0
+    assert call(e_=bad) == B.SURR_E_INVALID_ARG
+    assert L.surrogate_evaluate(None, p, 10, 8, m.ctypes.data, e.ctypes.data, c.ctypes.data, 1, p,
+                                1 << 20, None, None, None, p, None) == B.SURR_E_INVALID_ARG
 
 
 def test_score_pairs_rejects_null_model():
