@@ -191,6 +191,62 @@ def prefix_reuse_rates(B, torch, dev, model, steps: int, warmup: int) -> dict:
                     "prefix build per batch; plain scores the concatenated prompts"}
 
 
+def decode_rates(B, torch, dev, model, s, tok_np, L, steps: int = 32,
+                 in_flight=(8, 32, 128), prompt_cap: int = 2048) -> dict:
+    """Greedy decode throughput against the number of sequences in flight (the paper's
+    surrogate reasons before its verdict).  For each P: the first P prompts of the
+    workload, cut to prompt_cap tokens, are prefilled into cache entries (untimed); then
+    `steps` decode steps, each appending every sequence's greedy token, are timed with
+    HIP events.  Algorithmic HBM bytes per step: every weight matrix once, the entries'
+    cached keys and values once, the new keys and values written once."""
+    d, dq, dkv, ff, nl, V = s.d_model, s.d_q, s.d_kv, s.d_ff, s.n_layers, s.vocab
+    esz = 2 if s.dtype == "bf16" else 4
+    w_bytes = esz * (nl * (d * (dq + 2 * dkv) + dq * d + 3 * d * ff) + V * d)
+    stream = torch.cuda.current_stream()
+    out = {"steps": steps, "prompt_cap": prompt_cap, "points": []}
+    for P in in_flight:
+        Lp = np.minimum(L[:P], prompt_cap).astype(np.int32)
+        cache = B.surrogate_cache_create(model, Lp + steps + 4)
+        ids = np.arange(P, dtype=np.int32)
+        tok = torch.from_numpy(np.ascontiguousarray(tok_np[:P, : int(Lp.max())])).to(dev)
+        ws = torch.empty(B.surrogate_workspace_size(model, P, int(Lp.sum()), int(Lp.max())),
+                         dtype=torch.uint8, device=dev)
+        nxt = torch.empty(P, dtype=torch.int32, device=dev)
+        B.surrogate_cache_extend(model, cache, ids, tok, Lp, ws, next_token=nxt, stream=stream)
+        del ws
+        ws = torch.empty(B.surrogate_workspace_size(model, P, P, 1), dtype=torch.uint8, device=dev)
+        ones = np.ones(P, np.int32)
+        step_tok = nxt.view(P, 1)
+
+        def step():
+            B.surrogate_cache_extend(model, cache, ids, step_tok, ones, ws, next_token=nxt,
+                                     stream=stream)
+
+        for _ in range(2):
+            step()
+        torch.cuda.synchronize()
+        ctx0 = Lp.astype(np.float64) + 2
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / 1e3 / steps
+        kv_read = float(sum((ctx0.sum() + P * i) for i in range(steps))) / steps * nl * 2 * dkv * esz
+        kv_write = P * nl * 2 * dkv * esz
+        bytes_step = w_bytes + kv_read + kv_write
+        out["points"].append({"in_flight": P, "ms_per_step": t * 1e3, "tokens_per_s": P / t,
+                              "mean_context": float(ctx0.mean()) + steps / 2,
+                              "hbm_bytes_per_step": bytes_step,
+                              "achieved_GBps": bytes_step / t / 1e9,
+                              "frac_of_hbm": bytes_step / t / PEAK_HBM})
+        cache.close()
+        del ws, tok
+        torch.cuda.empty_cache()
+    return out
+
+
 def forecast_head_rates(B, torch, dev, n: int = 65536, reps: int = 200) -> dict:
     """Latency and achieved HBM rate of the eight-bin forecast head (expected speedup and
     three discovery cutoffs) and of top-quarter selection by expected speedup, on n
@@ -297,6 +353,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the per-phase HIP-event timing (the roofline block)")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the decode-throughput section (7B shape only)")
     ap.add_argument("--no-prefix", action="store_true",
                     help="skip the shared-prefix workload (7B shape only)")
     ap.add_argument("--no-forecast-head", action="store_true",
@@ -423,9 +481,16 @@ def main() -> int:
         out["phase_rates"] = phase_rates(s, L.astype(np.int64), phases, args.steps)
     if not args.no_forecast_head:
         out["forecast_head"] = forecast_head_rates(B, torch, dev)
+    if not args.no_decode and args.config == "7b":
+        print("[bench] decode throughput", file=sys.stderr, flush=True)
+        if "ws" in locals():
+            del ws
+        torch.cuda.empty_cache()
+        out["decode"] = decode_rates(B, torch, dev, model, s, tok_np, L)
     if not args.no_prefix and args.config == "7b":
         print("[bench] shared-prefix workload", file=sys.stderr, flush=True)
-        del ws
+        if "ws" in locals():
+            del ws
         torch.cuda.empty_cache()
         out["prefix_reuse"] = prefix_reuse_rates(B, torch, dev, model, max(1, min(args.steps, 3)),
                                                  1)

@@ -168,6 +168,41 @@ surrogate_status surrogate_score_suffixes(surrogate_model *m, const surrogate_pr
                                           float *probs_d, float *confidence_d, int32_t *verdict_d,
                                           hipStream_t stream);
 
+/* Decode continuation.  A cache also holds growing token sequences: entries with a
+ * reserved capacity whose keys and values are appended by prefill and decode steps.
+ * surrogate_cache_create reserves n_entries entries of capacity_h[g] tokens (1 <=
+ * capacity <= max_pos; rounded up to 64), all empty, in device memory the cache owns
+ * (cleared; synchronous).  surrogate_cache_extend appends lengths_h[i] tokens (tokens_d
+ * [batch, row_stride], device) to entry entry_ids_h[i] for every i, with positions
+ * continuing the entry (length + lengths_h[i] <= min(capacity, max_pos); an entry at
+ * most once per call): the tokens attend to everything the entry held before and
+ * causally to each other, exactly as the same tokens at the end of one long prompt would.
+ * A prefill passes a whole prompt; a decode step passes one token per sequence.  After
+ * the last appended token of each entry it writes (device, caller-owned, either may be
+ * NULL) next_token_d[i], the first argmax of the next-token distribution over the
+ * vocabulary (greedy decoding), and target_logprob_d[i], its full-vocabulary log-softmax at
+ * target_ids_h[i] (host; teacher forcing).  The entry lengths advance when the call
+ * returns (the device work is stream-ordered behind it); surrogate_cache_lengths reads
+ * them and surrogate_cache_reset empties entries for reuse.  Workspace:
+ * surrogate_workspace_size(m, batch, sum of lengths_h, max of lengths_h).  A cache made
+ * by surrogate_prefix_build is an ordinary cache whose entries are full; any cache can
+ * serve as the prefixes of surrogate_score_suffixes.
+ * Errors: SURR_E_INVALID_ARG (nulls, entry or target ids out of range, an entry twice,
+ * a cache of another model), SURR_E_SHAPE (lengths past the capacity or max_pos),
+ * SURR_E_WORKSPACE, SURR_E_OOM, SURR_E_HIP. */
+surrogate_status surrogate_cache_create(surrogate_model *m, int32_t n_entries,
+                                        const int32_t *capacity_h, surrogate_prefix_cache **out);
+surrogate_status surrogate_cache_extend(surrogate_model *m, surrogate_prefix_cache *cache,
+                                        const int32_t *entry_ids_h, const int32_t *tokens_d,
+                                        int64_t row_stride, const int32_t *lengths_h,
+                                        int32_t batch, const int32_t *target_ids_h,
+                                        void *workspace_d, size_t workspace_bytes,
+                                        int32_t *next_token_d, float *target_logprob_d,
+                                        hipStream_t stream);
+surrogate_status surrogate_cache_lengths(const surrogate_prefix_cache *cache, int32_t *lengths_h);
+surrogate_status surrogate_cache_reset(surrogate_prefix_cache *cache, const int32_t *entry_ids_h,
+                                       int32_t n);
+
 /* Device bytes held by the cache. */
 surrogate_status surrogate_prefix_cache_bytes(const surrogate_prefix_cache *cache, size_t *bytes);
 

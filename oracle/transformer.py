@@ -132,6 +132,17 @@ def last_position_logits(arch, weights, xs) -> np.ndarray:
     return y @ to_f64(weights["lm_head"]).T
 
 
+def next_token_log_softmax(arch, weights, tokens, positions) -> np.ndarray:
+    """Full-vocabulary log-softmax of the next-token logits after each of `positions`
+    of one token sequence: row r is log p(. | tokens[0 .. positions[r]]).  The causal
+    forward makes every row the last-position read-out of the corresponding prefix."""
+    x = forward_hidden(arch, weights, [tokens])[0]
+    g = to_f64(weights["final_norm"])
+    y = np.stack([rms_norm(x[j], g, arch["rms_eps"]) for j in positions])
+    z = y @ to_f64(weights["lm_head"]).T
+    return np.stack([log_softmax_full(zi) for zi in z])
+
+
 def forecast(lp: np.ndarray) -> dict:
     """Verdict log-probs lp[B, n] -> p (renormalised), confidence q = max p,
     predicted verdict = first argmax, and the top-1 minus top-2 log-prob margin."""

@@ -30,7 +30,8 @@ EXPORTS = ("surrogate_tensor_count", "surrogate_tensor_shape", "surrogate_load_w
            "surrogate_status_string", "surrogate_last_error", "surrogate_profile_enable",
            "surrogate_profile_collect", "surrogate_forecast_head", "surrogate_prefix_build",
            "surrogate_score_suffixes", "surrogate_prefix_cache_bytes", "surrogate_prefix_free",
-           "surrogate_evaluate_workspace_size", "surrogate_evaluate")
+           "surrogate_evaluate_workspace_size", "surrogate_evaluate", "surrogate_cache_create",
+           "surrogate_cache_extend", "surrogate_cache_lengths", "surrogate_cache_reset")
 PHASES = ("embed", "rmsnorm", "gemm_qkv", "rope", "attention", "gemm_o", "gemm_gate_up",
           "gemm_down", "last_rows", "lm_head", "lse_verdict", "prefix_capture")
 
@@ -83,6 +84,10 @@ def lib() -> ctypes.CDLL:
         "surrogate_prefix_cache_bytes": (I32, [P, ctypes.POINTER(SZ)]),
         "surrogate_prefix_free": (None, [P]),
         "surrogate_evaluate_workspace_size": (I32, [I32, I32, ctypes.POINTER(SZ)]),
+        "surrogate_cache_create": (I32, [P, I32, P, ctypes.POINTER(P)]),
+        "surrogate_cache_extend": (I32, [P, P, P, P, I64, P, I32, P, P, SZ, P, P, P]),
+        "surrogate_cache_lengths": (I32, [P, P]),
+        "surrogate_cache_reset": (I32, [P, P, I32]),
         "surrogate_evaluate": (I32, [P, P, I32, I32, P, P, P, I32, P, SZ, P, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
@@ -224,6 +229,53 @@ class PrefixCache:
             self.close()
         except Exception:
             pass
+
+
+def surrogate_cache_create(model: Model, capacities) -> PrefixCache:
+    """Empty cache entries of the given token capacities (decode continuation)."""
+    cap = np.ascontiguousarray(np.asarray(capacities, dtype=np.int32))
+    h = ctypes.c_void_p()
+    _check(lib().surrogate_cache_create(model.handle, int(cap.size),
+                                        cap.ctypes.data_as(ctypes.c_void_p), ctypes.byref(h)),
+           "surrogate_cache_create")
+    return PrefixCache(h.value, np.zeros(cap.size, np.int32))
+
+
+def surrogate_cache_extend(model: Model, cache: PrefixCache, entry_ids, tokens, lengths, workspace,
+                           target_ids=None, next_token=None, target_logprob=None, stream=None):
+    """Append row i of tokens (int32 device [B, S], lengths[i] valid) to entry
+    entry_ids[i]; writes the greedy next token and, with target_ids, its log-prob."""
+    import torch
+    if tokens.dtype != torch.int32 or tokens.dim() != 2 or not tokens.is_contiguous():
+        raise ValueError("tokens must be a contiguous int32 [B, S] device tensor")
+    L = np.ascontiguousarray(np.asarray(lengths, dtype=np.int32))
+    eid = np.ascontiguousarray(np.asarray(entry_ids, dtype=np.int32))
+    B = int(tokens.shape[0])
+    if L.shape != (B,) or eid.shape != (B,):
+        raise ValueError("lengths and entry_ids must have one entry per row of tokens")
+    tgt = None if target_ids is None else np.ascontiguousarray(np.asarray(target_ids, dtype=np.int32))
+    if tgt is not None and tgt.shape != (B,):
+        raise ValueError("target_ids must have one entry per row of tokens")
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
+    _check(lib().surrogate_cache_extend(
+        model.handle, cache.handle, eid.ctypes.data_as(ctypes.c_void_p), ptr(tokens),
+        int(tokens.shape[1]), L.ctypes.data_as(ctypes.c_void_p), B,
+        tgt.ctypes.data_as(ctypes.c_void_p) if tgt is not None else None, ptr(workspace),
+        workspace.numel() * workspace.element_size(), ptr(next_token), ptr(target_logprob),
+        ctypes.c_void_p(_stream(stream))), "surrogate_cache_extend")
+
+
+def surrogate_cache_lengths(cache: PrefixCache, n_entries: int) -> np.ndarray:
+    out = np.zeros(n_entries, np.int32)
+    _check(lib().surrogate_cache_lengths(cache.handle, out.ctypes.data_as(ctypes.c_void_p)),
+           "surrogate_cache_lengths")
+    return out
+
+
+def surrogate_cache_reset(cache: PrefixCache, entry_ids):
+    eid = np.ascontiguousarray(np.asarray(entry_ids, dtype=np.int32))
+    _check(lib().surrogate_cache_reset(cache.handle, eid.ctypes.data_as(ctypes.c_void_p),
+                                       int(eid.size)), "surrogate_cache_reset")
 
 
 def surrogate_prefix_build(model: Model, tokens, lengths, workspace, stream=None) -> PrefixCache:
@@ -415,6 +467,22 @@ class Scorer:
         L = np.asarray(lengths, np.int32)
         ws = self.ensure_workspace(len(L), int(L.sum()), int(L.max()))
         return surrogate_prefix_build(self.model, tok, L, ws)
+
+    def create_cache(self, capacities) -> PrefixCache:
+        return surrogate_cache_create(self.model, capacities)
+
+    def extend(self, cache: PrefixCache, entry_ids, tokens, lengths, target_ids=None):
+        """Append tokens to cache entries; returns (next_token, target_logprob or None)."""
+        torch = self.torch
+        tok = torch.as_tensor(np.asarray(tokens, np.int32)).to(self.device) \
+            if not isinstance(tokens, torch.Tensor) else tokens
+        L = np.asarray(lengths, np.int32)
+        B = len(L)
+        ws = self.ensure_workspace(B, int(L.sum()), int(L.max()))
+        nxt = torch.empty(B, dtype=torch.int32, device=self.device)
+        lp = torch.empty(B, dtype=torch.float32, device=self.device) if target_ids is not None else None
+        surrogate_cache_extend(self.model, cache, entry_ids, tok, L, ws, target_ids, nxt, lp)
+        return nxt, lp
 
     def score_suffixes(self, cache: PrefixCache, prefix_ids, tokens, lengths, verdict_ids):
         torch = self.torch

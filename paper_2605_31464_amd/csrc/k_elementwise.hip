@@ -258,6 +258,93 @@ __global__ __launch_bounds__(256) void capture_rows_kernel(const uint32_t* __res
     }
 }
 
+// ---------------------------------------------------------------- sequence caches
+// Token j of prompt b (packed row t = cu[b] + j) continues its sequence at position
+// len[b] + j: columns [col0, col0 + words) of row t go to cache row off[b] + len[b] + j.
+__global__ __launch_bounds__(256) void append_rows_kernel(const uint32_t* __restrict__ src,
+                                                          int64_t ld_src, int col0, int words,
+                                                          const int32_t* __restrict__ cu, int B,
+                                                          const int32_t* __restrict__ off,
+                                                          const int32_t* __restrict__ len,
+                                                          uint32_t* __restrict__ dst,
+                                                          int64_t ld_dst) {
+    const int64_t t = blockIdx.x;
+    int lo = 0, hi = B;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (cu[mid] <= t) lo = mid; else hi = mid;
+    }
+    const int64_t r = (int64_t)off[lo] + len[lo] + (t - cu[lo]);
+    const uint32_t* sr = src + t * ld_src + col0;
+    uint32_t* o = dst + r * ld_dst;
+    for (int c = threadIdx.x; c < words; c += 256) o[c] = sr[c];
+}
+
+// Transposed V of the same tokens: column vt_off[b] + pi(j) of vt goes to column
+// off[b] + pi(len[b] + j) of the cache's V^T (pi = vt_key_order, applied to the index
+// inside the 64-aligned block of each side).  Block (b, 64-token chunk), threads over rows.
+__global__ __launch_bounds__(256) void append_vt_kernel(const uint16_t* __restrict__ vt,
+                                                        int64_t ld_vt,
+                                                        const int32_t* __restrict__ vt_off,
+                                                        const int32_t* __restrict__ cu,
+                                                        const int32_t* __restrict__ off,
+                                                        const int32_t* __restrict__ len,
+                                                        int rows, uint16_t* __restrict__ cvt,
+                                                        int64_t ld_c) {
+    const int b = blockIdx.x, j0 = blockIdx.y * 64;
+    const int L = cu[b + 1] - cu[b];
+    if (j0 >= L) return;
+    const int jn = min(64, L - j0), base = len[b];
+    for (int d = threadIdx.x; d < rows; d += 256) {
+        const uint16_t* sr = vt + (int64_t)d * ld_vt + vt_off[b];
+        uint16_t* o = cvt + (int64_t)d * ld_c + off[b];
+        for (int j = j0; j < j0 + jn; ++j) o[vt_key_order(base + j)] = sr[vt_key_order(j)];
+    }
+}
+
+// Next-token read-out per row of logits: LSE over the vocabulary (same order of
+// operations as lse_verdict_kernel), the first argmax, and optionally the log-prob of a
+// given target id.
+__global__ __launch_bounds__(256) void lse_next_kernel(const float* __restrict__ logits, int64_t ld,
+                                                       int V, const int32_t* __restrict__ target,
+                                                       int32_t* __restrict__ next_token,
+                                                       float* __restrict__ target_lp) {
+    __shared__ float red[4];
+    __shared__ int redi[4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int b = blockIdx.x;
+    const float* z = logits + (int64_t)b * ld;
+    float mx = -INFINITY;
+    int am = V;
+    for (int i = tid; i < V; i += 256) {
+        const float v = z[i];
+        if (v > mx) { mx = v; am = i; }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {  // larger value wins, the lower index on ties
+        const float ov = __shfl_xor(mx, o, 64);
+        const int oi = __shfl_xor(am, o, 64);
+        if (ov > mx || (ov == mx && oi < am)) { mx = ov; am = oi; }
+    }
+    if (lane == 0) { red[wave] = mx; redi[wave] = am; }
+    __syncthreads();
+    mx = red[0];
+    am = redi[0];
+    for (int w = 1; w < 4; ++w)
+        if (red[w] > mx || (red[w] == mx && redi[w] < am)) { mx = red[w]; am = redi[w]; }
+    __syncthreads();
+    float s = 0.f;
+    for (int i = tid; i < V; i += 256) s += expf(z[i] - mx);
+    s = wave_sum(s);
+    if (lane == 0) red[wave] = s;
+    __syncthreads();
+    if (tid == 0) {
+        const float lse = mx + logf(((red[0] + red[1]) + red[2]) + red[3]);
+        if (next_token) next_token[b] = am;
+        if (target_lp) target_lp[b] = z[target[b]] - lse;
+    }
+}
+
 // ---------------------------------------------------------------- LSE + verdicts
 // One workgroup per prompt.  LSE = max + log(sum exp(z - max)) over the full vocabulary
 // (fixed-order reductions), lp_v = z[vid_v] - LSE, then p = softmax(lp), q = max p and
@@ -571,6 +658,32 @@ hipError_t launch_lse_verdict(const float* logits, int64_t ld, int B, int V, con
                               int nv, float* lp, float* probs, float* conf, int32_t* verdict,
                               hipStream_t s) {
     lse_verdict_kernel<<<B, 256, 0, s>>>(logits, ld, V, vid, nv, lp, probs, conf, verdict);
+    return hipGetLastError();
+}
+
+hipError_t launch_append_rows(const void* src, int64_t ld_src, int col0, int cols, int elem_bytes,
+                              int64_t T, const int32_t* cu, int B, const int32_t* off,
+                              const int32_t* len, void* dst, int64_t ld_dst, hipStream_t s) {
+    if (T == 0) return hipSuccess;
+    append_rows_kernel<<<(unsigned)T, 256, 0, s>>>(
+        static_cast<const uint32_t*>(src), ld_src * elem_bytes / 4, col0 * elem_bytes / 4,
+        cols * elem_bytes / 4, cu, B, off, len, static_cast<uint32_t*>(dst), ld_dst * elem_bytes / 4);
+    return hipGetLastError();
+}
+
+hipError_t launch_append_vt(const uint16_t* vt, int64_t ld_vt, const int32_t* vt_off,
+                            const int32_t* cu, int B, int max_len, const int32_t* off,
+                            const int32_t* len, int rows, uint16_t* cvt, int64_t ld_c,
+                            hipStream_t s) {
+    if (B == 0 || max_len == 0) return hipSuccess;
+    append_vt_kernel<<<dim3(B, (max_len + 63) / 64), 256, 0, s>>>(vt, ld_vt, vt_off, cu, off, len,
+                                                                 rows, cvt, ld_c);
+    return hipGetLastError();
+}
+
+hipError_t launch_lse_next(const float* logits, int64_t ld, int B, int V, const int32_t* target,
+                           int32_t* next_token, float* target_lp, hipStream_t s) {
+    lse_next_kernel<<<B, 256, 0, s>>>(logits, ld, V, target, next_token, target_lp);
     return hipGetLastError();
 }
 

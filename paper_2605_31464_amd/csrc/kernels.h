@@ -55,6 +55,24 @@ hipError_t launch_lse_verdict(const float* logits, int64_t ld, int B, int V, con
                               int nv, float* lp, float* probs, float* conf, int32_t* verdict,
                               hipStream_t s);
 
+// Sequence caches: the packed tokens (prompt b's token j at row cu[b] + j) continue their
+// sequences at positions len[b] + j.  append_rows copies columns [col0, col0 + cols) of
+// each row to cache row off[b] + len[b] + j; append_vt copies the transposed V columns
+// vt_off[b] + vt_key_order(j) to cache columns off[b] + vt_key_order(len[b] + j) for the
+// `rows` rows of V^T (max_len: the longest prompt).
+hipError_t launch_append_rows(const void* src, int64_t ld_src, int col0, int cols, int elem_bytes,
+                              int64_t T, const int32_t* cu, int B, const int32_t* off,
+                              const int32_t* len, void* dst, int64_t ld_dst, hipStream_t s);
+hipError_t launch_append_vt(const uint16_t* vt, int64_t ld_vt, const int32_t* vt_off,
+                            const int32_t* cu, int B, int max_len, const int32_t* off,
+                            const int32_t* len, int rows, uint16_t* cvt, int64_t ld_c,
+                            hipStream_t s);
+
+// Per row of logits: the first argmax over the vocabulary (next_token, optional) and the
+// full-vocabulary log-softmax at target[b] (target_lp, optional).
+hipError_t launch_lse_next(const float* logits, int64_t ld, int B, int V, const int32_t* target,
+                           int32_t* next_token, float* target_lp, hipStream_t s);
+
 // Selection and ordered compaction in one workgroup, 1 <= n <= 65536.  mode 0: defer
 // !(q >= tau); mode 1: defer the k lowest (NaN first); mode 2: defer the k highest (NaN
 // last); ties by ascending index.

@@ -47,7 +47,7 @@ struct LayerW {
 
 // Byte offsets of one call's workspace regions.
 struct WsLayout {
-    size_t cu, last, vid, work, work_last, vt_off, pfx_len, pfx_off, pos, vcol, x, h, qkv, vt, o,
+    size_t cu, last, vid, work, work_last, vt_off, pfx_len, pfx_off, target, pos, vcol, x, h, qkv, vt, o,
         u, gu, o_last, x_last, h_last, u_last, gu_last, y, logits, total;
     int64_t ld_vt;  // columns of the transposed V copy (bf16 models)
 };
@@ -121,13 +121,15 @@ struct surrogate_model {
     int64_t d_qkv() const { return d_q() + 2 * d_kv(); }
 };
 
-// Keys (after RoPE) and values of every layer for a set of shared prompt prefixes.
-// Prefix g owns rows [off[g], off[g] + roundup(len[g], 64)) of each layer's K [rows][d_kv]
-// and the same range of its V: bf16 stores V transposed ([d_kv][rows], keys of each
-// 16-key group in the order of the kernels' V^T copy), fp32 stores V rows [rows][d_kv].
+// Keys (after RoPE) and values of every layer for a set of token sequences: shared prompt
+// prefixes, or sequences that grow by prefill and decode steps.  Entry g owns rows
+// [off[g], off[g] + cap[g]) (cap a multiple of 64) of each layer's K [rows][d_kv] and the
+// same range of its V: bf16 stores V transposed ([d_kv][rows], keys of each 16-key group
+// in the order of the kernels' V^T copy), fp32 stores V rows [rows][d_kv].  The first
+// len[g] rows hold the entry's tokens; the rest are zero or stale (never read unmasked).
 struct surrogate_prefix_cache {
     const surrogate_model* model = nullptr;
-    std::vector<int32_t> len, off;
+    std::vector<int32_t> len, off, cap;
     int64_t rows = 0;
     char* mem = nullptr;
     size_t k_bytes = 0, v_bytes = 0;  // per layer
@@ -154,6 +156,7 @@ WsLayout layout(const surrogate_model* m, int64_t B, int64_t T) {
     w.vt_off = take(4 * (B + 1));
     w.pfx_len = take(4 * B);
     w.pfx_off = take(4 * B);
+    w.target = take(4 * B);
     w.pos = take(4 * T);
     // Transposed V copy: every prompt's keys start on a 64-column boundary, so its
     // padded ranges need at most T + 63 B columns.
@@ -188,6 +191,10 @@ struct PassIO {
     surrogate_prefix_cache* capture = nullptr;
     const surrogate_prefix_cache* prefix = nullptr;  // prompts continue cached prefixes
     const int32_t* prefix_id_h = nullptr;            // per prompt: prefix index or -1
+    surrogate_prefix_cache* append = nullptr;  // prompts extend these entries (prefix_id_h)
+    const int32_t* target_ids_h = nullptr;     // per prompt: next-token id to score
+    int32_t* next_token_d = nullptr;           // per prompt: first argmax of the next token
+    float* target_lp_d = nullptr;              // per prompt: log-softmax at target_ids_h
     const int32_t* verdict_ids_h = nullptr;
     int32_t n_verdict = 0;
     float* logprobs_d = nullptr;
@@ -212,25 +219,39 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
     const surrogate_config& c = m->cfg;
     if (batch < 1) return fail(SURR_E_INVALID_ARG, "batch must be >= 1");
     if (row_stride < 1) return fail(SURR_E_INVALID_ARG, "row_stride must be >= 1");
-    std::vector<int32_t> plen(batch, 0), poff(batch, 0);
+    std::vector<int32_t> plen(batch, 0), poff(batch, 0), room(batch, INT32_MAX);
     if (io.prefix) {
         const int np = (int)io.prefix->len.size();
+        std::vector<char> seen(np, 0);
         for (int b = 0; b < batch; ++b) {
             const int g = io.prefix_id_h[b];
-            if (g < -1 || g >= np) return fail(SURR_E_INVALID_ARG, "prefix id of prompt " + std::to_string(b) + " outside [-1, n_prefix)");
+            if (g < (io.append ? 0 : -1) || g >= np)
+                return fail(SURR_E_INVALID_ARG, "entry id of prompt " + std::to_string(b) + (io.append ? " outside [0, n_entries)" : " outside [-1, n_prefix)"));
             if (g >= 0) {
                 plen[b] = io.prefix->len[g];
                 poff[b] = io.prefix->off[g];
+                if (io.append) {
+                    if (seen[g]) return fail(SURR_E_INVALID_ARG, "entry " + std::to_string(g) + " appears twice in one call");
+                    seen[g] = 1;
+                    room[b] = io.prefix->cap[g] - plen[b];
+                }
             }
         }
     }
+    if (io.target_ids_h)
+        for (int b = 0; b < batch; ++b)
+            if (io.target_ids_h[b] < 0 || io.target_ids_h[b] >= c.vocab)
+                return fail(SURR_E_INVALID_ARG, "target id of prompt " + std::to_string(b) + " outside [0, vocab)");
     // a prompt's positions run to prefix length + length - 1 < max_pos; a prefix leaves
     // room for at least one continuing token
     int64_t T = 0;
+    int max_len = 0;
     for (int b = 0; b < batch; ++b) {
-        const int64_t cap = std::min<int64_t>(row_stride, (int64_t)c.max_pos - plen[b] - (io.build ? 1 : 0));
+        max_len = std::max(max_len, lengths_h[b]);
+        const int64_t cap = std::min<int64_t>(std::min<int64_t>(row_stride, room[b]),
+                                              (int64_t)c.max_pos - plen[b] - (io.build ? 1 : 0));
         if (lengths_h[b] < 1 || lengths_h[b] > cap)
-            return fail(SURR_E_SHAPE, "length of prompt " + std::to_string(b) + (io.build ? " outside [1, min(row_stride, max_pos - 1)]" : io.prefix ? " outside [1, min(row_stride, max_pos - prefix length)]" : " outside [1, min(row_stride, max_pos)]"));
+            return fail(SURR_E_SHAPE, "length of prompt " + std::to_string(b) + (io.build ? " outside [1, min(row_stride, max_pos - 1)]" : io.append ? " outside [1, min(row_stride, max_pos - length, capacity - length)]" : io.prefix ? " outside [1, min(row_stride, max_pos - prefix length)]" : " outside [1, min(row_stride, max_pos)]"));
         T += lengths_h[b];
     }
     if (T + 64 * (int64_t)batch > INT32_MAX)
@@ -289,6 +310,7 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
         std::memcpy(P + w.vt_off, vt_off.data(), 4 * vt_off.size());
         std::memcpy(P + w.pfx_len, plen.data(), 4 * plen.size());
         std::memcpy(P + w.pfx_off, poff.data(), 4 * poff.size());
+        if (io.target_ids_h) std::memcpy(P + w.target, io.target_ids_h, 4 * (size_t)batch);
         SURR_HIP(hipMemcpyAsync(workspace_d, P, meta_bytes, hipMemcpyHostToDevice, stream));
         SURR_HIP(hipEventRecord(m->staged, stream));
         m->staged_pending = true;
@@ -304,6 +326,7 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
     const int32_t* d_po = reinterpret_cast<const int32_t*>(W + w.vt_off);  // 64-aligned row blocks
     const int32_t* d_pfx_len = reinterpret_cast<const int32_t*>(W + w.pfx_len);
     const int32_t* d_pfx_off = reinterpret_cast<const int32_t*>(W + w.pfx_off);
+    const int32_t* d_target = reinterpret_cast<const int32_t*>(W + w.target);
     const bool bf16 = m->act == Act::BF16;
     const int32_t* d_vt_off = bf16 ? reinterpret_cast<const int32_t*>(W + w.vt_off) : nullptr;
     int32_t* d_vcol = bf16 ? reinterpret_cast<int32_t*>(W + w.vcol) : nullptr;
@@ -407,6 +430,17 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
                 SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, surr::launch_capture_rows(qkv, dqkv, dq + (int)m->d_kv(), (int)m->d_kv(), 4, d_cu, d_po, batch, pc->rows, pc->v(l), m->d_kv(), stream));
             if (final_layer) break;  // nothing past the last layer's K/V is needed
         }
+        if (io.append) {
+            // the new tokens' keys and values continue their entries (rows past the
+            // entries' current lengths, which this layer's attention does not read)
+            surrogate_prefix_cache* pc = io.append;
+            const int dkv = (int)m->d_kv();
+            SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, surr::launch_append_rows(qkv, dqkv, dq, dkv, (int)m->esz, T, d_cu, batch, d_pfx_off, d_pfx_len, pc->k(l), dkv, stream));
+            if (bf16)
+                SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, surr::launch_append_vt(vt, w.ld_vt, d_vt_off, d_cu, batch, max_len, d_pfx_off, d_pfx_len, dkv, static_cast<uint16_t*>(pc->v(l)), pc->rows, stream));
+            else
+                SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, surr::launch_append_rows(qkv, dqkv, dq + dkv, dkv, 4, T, d_cu, batch, d_pfx_off, d_pfx_len, pc->v(l), dkv, stream));
+        }
         if (!final_layer) {
             SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, vt, w.ld_vt, d_vt_off, o, dq, d_cu, d_work, (int)work.size(), nq, nkv, hd, stream, pkp));
             SURR_PHASE_RUN(SURR_PHASE_GEMM_O, surr::launch_gemm(a, Epi::ResidAddF32, o, dq, L.w_o, dq, x, d, Ti, d, dq, stream));
@@ -428,8 +462,13 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
     if (io.build) return SURR_OK;
     SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, m->final_norm, d, c.rms_eps, y, d, stream));
     SURR_PHASE_RUN(SURR_PHASE_LM_HEAD, surr::launch_gemm(a, Epi::StoreF32, y, d, m->lm_head, d, logits, c.vocab, batch, c.vocab, d, stream));
-    SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_verdict(logits, c.vocab, batch, c.vocab, d_vid, n_verdict, logprobs_d, probs_d, confidence_d, verdict_d, stream));
+    if (n_verdict)
+        SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_verdict(logits, c.vocab, batch, c.vocab, d_vid, n_verdict, logprobs_d, probs_d, confidence_d, verdict_d, stream));
+    if (io.next_token_d || io.target_lp_d)
+        SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_next(logits, c.vocab, batch, c.vocab, io.target_ids_h ? d_target : nullptr, io.next_token_d, io.target_ids_h ? io.target_lp_d : nullptr, stream));
 #undef SURR_PHASE_RUN
+    if (io.append)  // the work above is enqueued: the entries now hold the new tokens
+        for (int b = 0; b < batch; ++b) io.append->len[io.prefix_id_h[b]] += lengths_h[b];
     return SURR_OK;
 }
 
@@ -618,9 +657,11 @@ surrogate_status surrogate_prefix_build(surrogate_model* m, const int32_t* token
     pc->model = m;
     pc->len.assign(lengths_h, lengths_h + n_prefix);
     pc->off.resize(n_prefix);
+    pc->cap.resize(n_prefix);
     for (int g = 0; g < n_prefix; ++g) {
         pc->off[g] = (int32_t)pc->rows;
-        pc->rows += (std::max(lengths_h[g], 0) + 63) / 64 * 64;
+        pc->cap[g] = (std::max(lengths_h[g], 0) + 63) / 64 * 64;
+        pc->rows += pc->cap[g];
     }
     // 32-bit DMA offsets over one kv head's V^T rows of the cache
     if (pc->rows * m->cfg.head_dim * 2 > (int64_t)UINT32_MAX || pc->rows > INT32_MAX) {
@@ -680,6 +721,83 @@ surrogate_status surrogate_score_suffixes(surrogate_model* m, const surrogate_pr
     io.probs_d = probs_d;
     io.confidence_d = confidence_d;
     io.verdict_d = verdict_d;
+    return run_pass(m, tokens_d, row_stride, lengths_h, batch, workspace_d, workspace_bytes, io, stream);
+}
+
+surrogate_status surrogate_cache_create(surrogate_model* m, int32_t n_entries,
+                                        const int32_t* capacity_h, surrogate_prefix_cache** out) {
+    if (!m || !capacity_h || !out) return fail(SURR_E_INVALID_ARG, "null argument");
+    *out = nullptr;
+    if (n_entries < 1) return fail(SURR_E_INVALID_ARG, "n_entries must be >= 1");
+    auto* pc = new surrogate_prefix_cache();
+    pc->model = m;
+    pc->len.assign(n_entries, 0);
+    pc->off.resize(n_entries);
+    pc->cap.resize(n_entries);
+    for (int g = 0; g < n_entries; ++g) {
+        if (capacity_h[g] < 1 || capacity_h[g] > m->cfg.max_pos) {
+            delete pc;
+            return fail(SURR_E_SHAPE, "capacity of entry " + std::to_string(g) + " outside [1, max_pos]");
+        }
+        pc->off[g] = (int32_t)pc->rows;
+        pc->cap[g] = (capacity_h[g] + 63) / 64 * 64;
+        pc->rows += pc->cap[g];
+    }
+    if (pc->rows * m->cfg.head_dim * 2 > (int64_t)UINT32_MAX || pc->rows > INT32_MAX) {
+        delete pc;
+        return fail(SURR_E_SHAPE, "entries too long for one cache");
+    }
+    pc->k_bytes = align_up((size_t)pc->rows * m->d_kv() * m->esz);
+    pc->v_bytes = pc->k_bytes;
+    const size_t bytes = (size_t)m->cfg.n_layers * (pc->k_bytes + pc->v_bytes);
+    if (hipMalloc(&pc->mem, bytes) != hipSuccess) {
+        delete pc;
+        return fail(SURR_E_OOM, "cache of " + std::to_string(bytes) + " bytes");
+    }
+    // masked rows past an entry's length are still multiplied: they must be finite
+    if (hipMemset(pc->mem, 0, bytes) != hipSuccess) {
+        hipFree(pc->mem);
+        delete pc;
+        return fail(SURR_E_HIP, "clearing the cache");
+    }
+    *out = pc;
+    return SURR_OK;
+}
+
+surrogate_status surrogate_cache_lengths(const surrogate_prefix_cache* cache, int32_t* lengths_h) {
+    if (!cache || !lengths_h) return fail(SURR_E_INVALID_ARG, "null argument");
+    std::copy(cache->len.begin(), cache->len.end(), lengths_h);
+    return SURR_OK;
+}
+
+surrogate_status surrogate_cache_reset(surrogate_prefix_cache* cache, const int32_t* entry_ids_h,
+                                       int32_t n) {
+    if (!cache || (n > 0 && !entry_ids_h)) return fail(SURR_E_INVALID_ARG, "null argument");
+    for (int i = 0; i < n; ++i)
+        if (entry_ids_h[i] < 0 || entry_ids_h[i] >= (int)cache->len.size())
+            return fail(SURR_E_INVALID_ARG, "entry id outside [0, n_entries)");
+    for (int i = 0; i < n; ++i) cache->len[entry_ids_h[i]] = 0;
+    return SURR_OK;
+}
+
+surrogate_status surrogate_cache_extend(surrogate_model* m, surrogate_prefix_cache* cache,
+                                        const int32_t* entry_ids_h, const int32_t* tokens_d,
+                                        int64_t row_stride, const int32_t* lengths_h,
+                                        int32_t batch, const int32_t* target_ids_h,
+                                        void* workspace_d, size_t workspace_bytes,
+                                        int32_t* next_token_d, float* target_logprob_d,
+                                        hipStream_t stream) {
+    if (!m || !cache || !entry_ids_h || !tokens_d || !lengths_h || !workspace_d)
+        return fail(SURR_E_INVALID_ARG, "null argument");
+    if (cache->model != m) return fail(SURR_E_INVALID_ARG, "cache was created for another model");
+    if (target_logprob_d && !target_ids_h) return fail(SURR_E_INVALID_ARG, "target log-probs need target ids");
+    PassIO io;
+    io.prefix = cache;
+    io.append = cache;
+    io.prefix_id_h = entry_ids_h;
+    io.target_ids_h = target_ids_h;
+    io.next_token_d = next_token_d;
+    io.target_lp_d = target_logprob_d;
     return run_pass(m, tokens_d, row_stride, lengths_h, batch, workspace_d, workspace_bytes, io, stream);
 }
 

@@ -23,7 +23,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = B.lib()
     names = declared_functions()
-    assert len(names) == 20
+    assert len(names) == 24
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B.EXPORTS)
@@ -152,6 +152,19 @@ def test_evaluate_rejects_bad_arguments_synchronously():
     assert call(e_=bad) == B.SURR_E_INVALID_ARG
     assert L.surrogate_evaluate(None, p, 10, 8, m.ctypes.data, e.ctypes.data, c.ctypes.data, 1, p,
                                 1 << 20, None, None, None, p, None) == B.SURR_E_INVALID_ARG
+
+
+def test_cache_calls_reject_bad_arguments_synchronously():
+    L = B.lib()
+    p = ctypes.c_void_p(256)
+    cap = np.array([64], np.int32)
+    h = ctypes.c_void_p()
+    assert L.surrogate_cache_create(None, 1, cap.ctypes.data, ctypes.byref(h)) == B.SURR_E_INVALID_ARG
+    lens = np.array([1], np.int32)
+    assert L.surrogate_cache_extend(None, p, lens.ctypes.data, p, 1, lens.ctypes.data, 1, None, p,
+                                    1 << 20, None, None, None) == B.SURR_E_INVALID_ARG
+    assert L.surrogate_cache_lengths(None, lens.ctypes.data) == B.SURR_E_INVALID_ARG
+    assert L.surrogate_cache_reset(None, lens.ctypes.data, 1) == B.SURR_E_INVALID_ARG
 
 
 def test_score_pairs_rejects_null_model():

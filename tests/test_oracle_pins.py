@@ -361,3 +361,18 @@ def test_paper_worked_values():
     for c in cases:
         d, a = osel.select_threshold(np.array([c["confidence"]], np.float32), c["tau"])
         assert bool(a.size) == c["accepted"], c["source"]
+
+
+# ---------------------------------------------------------------- next-token read-out
+def test_next_token_rows_equal_prefix_scoring():
+    """Row j of the teacher-forced read-out is the last-position read-out of the prefix
+    ending at j (the pinned scoring path), and each row is a distribution."""
+    arch, W = tiny_model(gain_std=0.1)
+    t = rand_prompt(512, 40, 11)
+    pos = [0, 7, 39]
+    rows = ot.next_token_log_softmax(arch, W, t, pos)
+    assert np.allclose(np.exp(rows).sum(axis=1), 1.0, atol=1e-12, rtol=0)
+    for r, j in enumerate(pos):
+        ids = [3, 100, 511]
+        ref = ot.score(arch, W, [t[: j + 1]], ids)["logprobs"][0]
+        assert np.allclose(rows[r, ids], ref, atol=1e-12, rtol=0)
