@@ -228,209 +228,146 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     // reaching its epilogue at once those partial-line writes run far below HBM rate.
     // Instead, once the LDS ring is idle, each fragment row i (32 rows of every row block)
     // is written to LDS in output layout and the workgroup then stores it in 16-byte
-    // chunks, each wavefront instruction covering whole 512- or 1024-byte row segments
-    // (the residual of ResidAddF32 is read the same way).  Tiles holding transposed V
-    // columns keep the direct path below.
-    {
-        constexpr bool F32OUT = EPI == Epi::StoreF32 || EPI == Epi::ResidAddF32;
-        constexpr int ESZ = F32OUT ? 4 : 2;
-        constexpr int OCOLS = EPI == Epi::SwiGLU ? BN / 2 : BN;  // output columns per tile
-        constexpr int PROWS = (BM / WM) * 32;                    // rows per pass
-        constexpr int PITCH = OCOLS * ESZ + 16;                  // staged row, bytes
-        constexpr int RCH = OCOLS * ESZ / 16;                    // 16-byte chunks per row
-        static_assert(PROWS * PITCH <= NST * S::STAGE * 16, "staging fits the LDS ring");
-        const bool staged = EPI != Epi::StoreActRope || n0 + BN <= rope.cols;
-        if (staged) {
-            char* stg = reinterpret_cast<char*>(lds);
-            const int rl = wm * 32 + (lane & 31);  // staged row of this lane
-            const int ncol0 = EPI == Epi::SwiGLU ? n0 / 2 : n0;
-            const int nlim = EPI == Epi::SwiGLU ? N / 2 : N;
-            __syncthreads();  // every wavefront is done with the ring
-#pragma unroll
-            for (int i = 0; i < S::FM; ++i) {
-                char* srow = stg + rl * PITCH;
-                if constexpr (EPI == Epi::SwiGLU) {
-#pragma unroll
-                    for (int j = 0; j < S::FN; j += 2)
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            float v[4];
-#pragma unroll
-                            for (int e = 0; e < 4; ++e)
-                                v[e] = silu(acc[i][j][4 * q + e]) * acc[i][j + 1][4 * q + e];
-                            const int col = (wn * WN + j * 32) / 2 + 8 * q + 4 * h;
-                            *reinterpret_cast<uint2*>(srow + col * 2) =
-                                make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
-                        }
-                } else if constexpr (EPI == Epi::StoreActRope) {
-                    static_assert(WN % 128 == 0, "wave tile must hold whole 128-dim heads");
-                    const int m = min(m0 + wm * WM + i * 32 + (lane & 31), M - 1);
-                    const int hd = rope.head_dim, half = hd >> 1, fstep = hd / 64;
-                    const float2* cs = rope.cs + (int64_t)rope.pos[m] * half;
-#pragma unroll
-                    for (int j = 0; j < S::FN; ++j) {
-                        const int cb = wn * WN + j * 32;  // tile column of the fragment
-                        if (((n0 + cb) % hd) >= half) continue;  // written with its partner
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const int col = cb + 8 * q + 4 * h;
-                            float v[4], w[4];
-#pragma unroll
-                            for (int e = 0; e < 4; ++e) {
-                                const float x1 = acc[i][j][4 * q + e];
-                                const float x2 = fstep == 1 ? acc[i][(j + 1) % S::FN][4 * q + e]
-                                                            : acc[i][(j + 2) % S::FN][4 * q + e];
-                                const float2 c = cs[(n0 + col + e) % hd];
-                                v[e] = x1 * c.x - x2 * c.y;
-                                w[e] = x2 * c.x + x1 * c.y;
-                            }
-                            *reinterpret_cast<uint2*>(srow + col * 2) =
-                                make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
-                            *reinterpret_cast<uint2*>(srow + (col + half) * 2) =
-                                make_uint2(pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3]));
-                        }
-                    }
-                } else {
-#pragma unroll
-                    for (int j = 0; j < S::FN; ++j)
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const int col = wn * WN + j * 32 + 8 * q + 4 * h;
-                            if constexpr (F32OUT) {
-                                *reinterpret_cast<f32x4*>(srow + col * 4) =
-                                    f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1],
-                                          acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-                            } else {
-                                *reinterpret_cast<uint2*>(srow + col * 2) = make_uint2(
-                                    pack_bf16x2(acc[i][j][4 * q], acc[i][j][4 * q + 1]),
-                                    pack_bf16x2(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]));
-                            }
-                        }
-                }
-                __syncthreads();
-                for (int c = tid; c < PROWS * RCH; c += S::THREADS) {
-                    const int rr = c / RCH, cc = c - rr * RCH;
-                    const int m = m0 + (rr >> 5) * WM + i * 32 + (rr & 31);
-                    const int n = ncol0 + cc * (16 / ESZ);
-                    if (m >= M || n >= nlim) continue;
-                    const uint4 v = *reinterpret_cast<const uint4*>(stg + rr * PITCH + cc * 16);
-                    char* g = static_cast<char*>(C) + ((int64_t)m * ldc + n) * ESZ;
-                    if constexpr (EPI == Epi::ResidAddF32) {
-                        f32x4* p = reinterpret_cast<f32x4*>(g);
-                        *p = *p + __builtin_bit_cast(f32x4, v);
-                    } else {
-                        *reinterpret_cast<uint4*>(g) = v;
-                    }
-                }
-                __syncthreads();
-            }
-            return;
-        }
-    }
-
+    // chunks, each wavefront instruction covering whole row segments (the residual of
+    // ResidAddF32 is read the same way).  The RoPE epilogue stages the fp32 accumulators:
+    // a chunk and its rotation partner (half a head away, in the same staged row) are
+    // combined at store time, so no wavefront needs to hold whole heads; columns of V
+    // heads are stored transposed, walking the staged block column by column so that a
+    // wavefront instruction writes 64 consecutive tokens of one row of V^T.
+    constexpr bool ROPE = EPI == Epi::StoreActRope;
+    constexpr bool F32OUT = EPI == Epi::StoreF32 || EPI == Epi::ResidAddF32;
+    constexpr int SESZ = (F32OUT || ROPE) ? 4 : 2;             // staged element size
+    constexpr int ESZ = F32OUT ? 4 : 2;                        // output element size
+    constexpr int OCOLS = EPI == Epi::SwiGLU ? BN / 2 : BN;    // output columns per tile
+    constexpr int PROWS = (BM / WM) * 32;                      // rows per pass
+    constexpr int PITCH = OCOLS * SESZ + 16;                   // staged row, bytes
+    constexpr int RCH = OCOLS * SESZ / 16;                     // 16-byte chunks per row
+    static_assert(PROWS * PITCH <= NST * S::STAGE * 16, "staging fits the LDS ring");
+    char* stg = reinterpret_cast<char*>(lds);
+    const int rl = wm * 32 + (lane & 31);  // staged row of this lane
+    const int ncol0 = EPI == Epi::SwiGLU ? n0 / 2 : n0;
+    const int nlim = EPI == Epi::SwiGLU ? N / 2 : N;
+    // RoPE tiles: columns [n0, rot_end) are rotated, [rot_end, n_end) are V columns
+    const int n_end = min(n0 + BN, N);
+    const int rot_end = ROPE ? max(n0, min(n_end, rope.cols)) : n_end;
+    const bool vt_cols = ROPE && rope.vt && rot_end < n_end;
+    __syncthreads();  // every wavefront is done with the ring
 #pragma unroll
     for (int i = 0; i < S::FM; ++i) {
-        const int m = m0 + wm * WM + i * 32 + (lane & 31);
-        if (m >= M) continue;
+        char* srow = stg + rl * PITCH;
         if constexpr (EPI == Epi::SwiGLU) {
-            // Fragment pairs (2p, 2p+1) hold gate and up rows of the same 32 outputs.
 #pragma unroll
-            for (int j = 0; j < S::FN; j += 2) {
-                const int nb = n0 + wn * WN + j * 32;
-                if (nb >= N) continue;
-                uint16_t* out = static_cast<uint16_t*>(C) + (int64_t)m * ldc + nb / 2;
+            for (int j = 0; j < S::FN; j += 2)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     float v[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         v[e] = silu(acc[i][j][4 * q + e]) * acc[i][j + 1][4 * q + e];
-                    uint2 o;
-                    o.x = pack_bf16x2(v[0], v[1]);
-                    o.y = pack_bf16x2(v[2], v[3]);
-                    *reinterpret_cast<uint2*>(out + 8 * q + 4 * h) = o;
+                    const int col = (wn * WN + j * 32) / 2 + 8 * q + 4 * h;
+                    *reinterpret_cast<uint2*>(srow + col * 2) =
+                        make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
                 }
-            }
-        } else if constexpr (EPI == Epi::StoreActRope) {
-            // Rotate-half RoPE on whole heads inside this wavefront's columns: the pair
-            // (i, i + hd/2) sits in fragments (j, j + hd/64) at the same lane position.
-            static_assert(WN % 128 == 0, "wave tile must hold whole 128-dim heads");
-            const int hd = rope.head_dim, half = hd >> 1, fstep = hd / 64;
-            const int pos = rope.pos[m];
-            const float2* cs = rope.cs + (int64_t)pos * half;
-            uint16_t* out = static_cast<uint16_t*>(C) + (int64_t)m * ldc;
+        } else {
 #pragma unroll
-            for (int j = 0; j < S::FN; ++j) {
-                const int nb = n0 + wn * WN + j * 32;
-                if (nb >= N) continue;
-                const bool rotated = nb < rope.cols;
-                const bool first_half = ((nb % hd) < half);
-                if (rotated && !first_half) continue;  // written together with its partner
+            for (int j = 0; j < S::FN; ++j)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int n = nb + 8 * q + 4 * h;
-                    float v[4], w[4];
-                    if (rotated) {
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            // partner fragment index: j + fstep (fstep = 1 for hd 64, 2 for hd 128)
-                            const float x1 = acc[i][j][4 * q + e];
-                            const float x2 = fstep == 1 ? acc[i][(j + 1) % S::FN][4 * q + e]
-                                                        : acc[i][(j + 2) % S::FN][4 * q + e];
-                            const float2 c = cs[(n + e) % hd];
-                            v[e] = x1 * c.x - x2 * c.y;
-                            w[e] = x2 * c.x + x1 * c.y;
-                        }
-                        uint2 o1, o2;
-                        o1.x = pack_bf16x2(v[0], v[1]);
-                        o1.y = pack_bf16x2(v[2], v[3]);
-                        o2.x = pack_bf16x2(w[0], w[1]);
-                        o2.y = pack_bf16x2(w[2], w[3]);
-                        *reinterpret_cast<uint2*>(out + n) = o1;
-                        *reinterpret_cast<uint2*>(out + n + half) = o2;
-                    } else if (rope.vt) {
-                        // V heads: transposed copy, column vcol[m] of rows n - cols
-                        const int64_t vc = rope.vcol[m];
-#pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            rope.vt[(int64_t)(n + e - rope.cols) * rope.ld_vt + vc] =
-                                (uint16_t)f32_to_bf16(acc[i][j][4 * q + e]);
+                    const int col = wn * WN + j * 32 + 8 * q + 4 * h;
+                    if constexpr (SESZ == 4) {
+                        *reinterpret_cast<f32x4*>(srow + col * 4) =
+                            f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                  acc[i][j][4 * q + 3]};
                     } else {
+                        *reinterpret_cast<uint2*>(srow + col * 2) = make_uint2(
+                            pack_bf16x2(acc[i][j][4 * q], acc[i][j][4 * q + 1]),
+                            pack_bf16x2(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]));
+                    }
+                }
+        }
+        __syncthreads();
+        if constexpr (ROPE) {
+            // Rotated q/k columns (and V columns when there is no transposed copy): a
+            // thread keeps one 4-column chunk and walks rows RSTEP apart; positions and
+            // cos/sin values of all its rows are loaded before any is used.
+            static_assert(S::THREADS % RCH == 0 && PROWS % (S::THREADS / RCH) == 0, "chunk walk");
+            constexpr int RSTEP = S::THREADS / RCH, NR = PROWS / RSTEP;
+            const int hd = rope.head_dim, half = hd >> 1;
+            const int lim = vt_cols ? rot_end : n_end;
+            const int cc = tid % RCH, r0 = tid / RCH;
+            const int n = n0 + cc * 4;
+            const int hi = n % hd;  // the 4 columns lie inside one half of a head
+            const bool lo = hi < half, rot = n < rope.cols;
+            const int poff = (lo ? half : -half) * 4;  // partner chunk, bytes
+            const int coff = lo ? hi : hi - half;
+            int mr[NR];
+            int pr[NR];
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
-                        uint2 o1;
-                        o1.x = pack_bf16x2(v[0], v[1]);
-                        o1.y = pack_bf16x2(v[2], v[3]);
-                        *reinterpret_cast<uint2*>(out + n) = o1;
+            for (int k = 0; k < NR; ++k) {
+                const int rr = r0 + k * RSTEP;
+                mr[k] = m0 + (rr >> 5) * WM + i * 32 + (rr & 31);
+                pr[k] = rot ? rope.pos[min(mr[k], M - 1)] : 0;
+            }
+            float4 cs[NR][2];
+#pragma unroll
+            for (int k = 0; k < NR; ++k) {
+                const float4* t = reinterpret_cast<const float4*>(rope.cs + (int64_t)pr[k] * half + coff);
+                cs[k][0] = rot ? t[0] : float4{1.f, 0.f, 1.f, 0.f};
+                cs[k][1] = rot ? t[1] : float4{1.f, 0.f, 1.f, 0.f};
+            }
+            if (n < lim) {
+#pragma unroll
+                for (int k = 0; k < NR; ++k) {
+                    const int rr = r0 + k * RSTEP;
+                    if (mr[k] >= M) continue;
+                    const char* sr = stg + rr * PITCH + cc * 16;
+                    const f32x4 x = *reinterpret_cast<const f32x4*>(sr);
+                    const f32x4 y = *reinterpret_cast<const f32x4*>(sr + poff);
+                    const float c4[4] = {cs[k][0].x, cs[k][0].z, cs[k][1].x, cs[k][1].z};
+                    const float s4[4] = {cs[k][0].y, cs[k][0].w, cs[k][1].y, cs[k][1].w};
+                    f32x4 r;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        // first half: x1 c - x2 s; second half: x2 c + x1 s (x1 = first-half value)
+                        r[e] = rot ? (lo ? x[e] * c4[e] - y[e] * s4[e] : x[e] * c4[e] + y[e] * s4[e]) : x[e];
+                    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(C) + (int64_t)mr[k] * ldc + n) =
+                        make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
+                }
+            }
+            if (vt_cols) {
+                // V columns, transposed: consecutive threads take consecutive tokens of one
+                // V dimension, i.e. consecutive columns of one row of V^T
+                static_assert(S::THREADS % PROWS == 0, "token walk");
+                const int rr = tid % PROWS;
+                const int m = m0 + (rr >> 5) * WM + i * 32 + (rr & 31);
+                if (m < M) {
+                    const int64_t vc = rope.vcol[m];
+                    for (int n2 = rot_end + tid / PROWS; n2 < n_end; n2 += S::THREADS / PROWS) {
+                        const float v = *reinterpret_cast<const float*>(stg + rr * PITCH + (n2 - n0) * 4);
+                        rope.vt[(int64_t)(n2 - rope.cols) * rope.ld_vt + vc] = (uint16_t)f32_to_bf16(v);
                     }
                 }
             }
         } else {
-#pragma unroll
-            for (int j = 0; j < S::FN; ++j) {
-                const int nb = n0 + wn * WN + j * 32;
-                if (nb >= N) continue;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int n = nb + 8 * q + 4 * h;
-                    const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                                     acc[i][j][4 * q + 3]};
-                    if constexpr (EPI == Epi::StoreAct) {
-                        uint2 o;
-                        o.x = pack_bf16x2(v[0], v[1]);
-                        o.y = pack_bf16x2(v[2], v[3]);
-                        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(C) + (int64_t)m * ldc + n) = o;
-                    } else if constexpr (EPI == Epi::StoreF32) {
-                        *reinterpret_cast<f32x4*>(static_cast<float*>(C) + (int64_t)m * ldc + n) = v;
-                    } else {
-                        f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(C) + (int64_t)m * ldc + n);
-                        *p = *p + v;
-                    }
+            for (int c = tid; c < PROWS * RCH; c += S::THREADS) {
+                const int rr = c / RCH, cc = c - rr * RCH;
+                const int m = m0 + (rr >> 5) * WM + i * 32 + (rr & 31);
+                const int n = ncol0 + cc * (16 / ESZ);
+                if (m >= M || n >= nlim) continue;
+                const uint4 v = *reinterpret_cast<const uint4*>(stg + rr * PITCH + cc * 16);
+                char* g = static_cast<char*>(C) + ((int64_t)m * ldc + n) * ESZ;
+                if constexpr (EPI == Epi::ResidAddF32) {
+                    f32x4* p = reinterpret_cast<f32x4*>(g);
+                    *p = *p + __builtin_bit_cast(f32x4, v);
+                } else {
+                    *reinterpret_cast<uint4*>(g) = v;
                 }
             }
         }
+        __syncthreads();
     }
 }
+
 
 #ifndef SURR_GEMM_KERNELS_ONLY  // (kernel-only builds for standalone tuning harnesses)
 template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI>
@@ -446,18 +383,13 @@ hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void
 // Tile choice (measured on the 7B projection shapes): 256 x 256 x 32 tiles, eight
 // wavefronts of 128 x 64 (two per SIMD, so one hides the other's waits), a 3-stage ring
 // and XCD-grouped order; 128 x 128 tiles for the few-row GEMMs of the last-position
-// head and the pruned final layer.  The RoPE epilogue uses wavefronts of 64 x 128 so
-// that each wavefront holds whole 128-wide heads.
+// head, the pruned final layer and decode steps.
 template <Epi EPI>
 hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                          int64_t ldc, int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
-    if constexpr (EPI == Epi::StoreActRope) {  // RoPE needs a wave tile of whole heads
-        return run_bf16<256, 256, 32, 64, 128, 3, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
-    } else {
-        if (M <= 128)
-            return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
-        return run_bf16<256, 256, 32, 128, 64, 3, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
-    }
+    if (M <= 128)
+        return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+    return run_bf16<256, 256, 32, 128, 64, 3, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
 }
 
 #endif  // SURR_GEMM_KERNELS_ONLY
