@@ -43,6 +43,13 @@ __device__ __forceinline__ int swz(int row) {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); }
 
+// Rotate-half RoPE of one value x with its partner y (the value half a head away) and
+// the angle's cos c and sin s: first half x c - y s, second half x c + y s.  Written
+// with explicit fused operations so every kernel rounds the same way.
+__device__ __forceinline__ float rope_rot(float x, float y, float c, float s, bool first_half) {
+    return first_half ? fmaf(x, c, -(y * s)) : fmaf(x, c, y * s);
+}
+
 // Tile order.  The hardware hands workgroup i to XCD i % 8, and each XCD has its own
 // L2.  With XCD remapping, XCD x receives the contiguous virtual range
 // [x * per_xcd, (x + 1) * per_xcd); virtual ids then walk GROUP M-tiles down before
@@ -329,7 +336,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         // first half: x1 c - x2 s; second half: x2 c + x1 s (x1 = first-half value)
-                        r[e] = rot ? (lo ? x[e] * c4[e] - y[e] * s4[e] : x[e] * c4[e] + y[e] * s4[e]) : x[e];
+                        r[e] = rot ? rope_rot(x[e], y[e], c4[e], s4[e], lo) : x[e];
                     *reinterpret_cast<uint2*>(static_cast<uint16_t*>(C) + (int64_t)mr[k] * ldc + n) =
                         make_uint2(pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]));
                 }
@@ -369,6 +376,186 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
 }
 
 
+
+// ---------------------------------------------------------------- few-row GEMM
+// C = A[M,K] * B[N,K]^T for M <= 16 MB rows (decode steps, last-position rows).  With so
+// few rows the work is reading B once, so each workgroup streams NF 16-row slices of B
+// over the whole K through a deep LDS ring (direct-to-LDS loads, up to ~60 KB in flight
+// per workgroup), together with the M rows of A; wavefront w < MB multiplies row block w
+// (v_mfma_f32_16x16x32_bf16).  Each output still accumulates k in ascending MFMA steps in
+// one fp32 accumulator, as in the tiled kernel (whose 32x32x16 steps give bitwise the same
+// sums), so a row's result does not depend on how many rows share the call.
+// The NF slices of workgroup g: plain epilogues one slice, rows [16 g, 16 g + 16); SwiGLU a
+// gate slice and its up slice 32 rows further (gate/up rows interleave in 32-row blocks);
+// RoPE a slice of the first half of a head and its partner half a head further, and, past
+// the rotated columns, two consecutive slices of V columns.
+template <int MB, int NF, Epi EPI>
+struct RowsCfg {
+    static constexpr int BK = 128, CH = BK / 8;          // 16-byte chunks per row and stage
+    static constexpr int ROWS_B = 16 * NF, ROWS_A = 16 * MB;
+    static constexpr int STAGE = (ROWS_B + ROWS_A) * CH;  // 16-byte slots per stage
+    static constexpr int THREADS = 256;
+    static constexpr int LOADS = STAGE / THREADS;
+    static constexpr int NST0 = 8192 / STAGE;             // 128 KB of ring
+    static constexpr int NST = NST0 > 16 ? 16 : NST0;
+    static_assert(STAGE % THREADS == 0 && (ROWS_B * CH) % 64 == 0, "whole wavefront loads");
+    static_assert(NST >= 3 && (NST - 2) * LOADS <= 63, "ring depth");
+    static_assert(MB <= 4, "one row block per wavefront");
+};
+
+template <int NF, Epi EPI>
+__device__ __forceinline__ int rows_slice(int g, int f, const RopeArgs& rope) {
+    if constexpr (EPI == Epi::SwiGLU) {
+        return 64 * (g >> 1) + 16 * (g & 1) + 32 * f;
+    } else if constexpr (EPI == Epi::StoreActRope) {
+        const int rot_groups = rope.cols / 32;
+        if (g < rot_groups) {
+            const int half = rope.head_dim >> 1, per_head = half / 16;
+            return (g / per_head) * rope.head_dim + 16 * (g % per_head) + half * f;
+        }
+        return rope.cols + 32 * (g - rot_groups) + 16 * f;
+    } else {
+        return 16 * (g * NF + f);
+    }
+}
+
+template <int MB, int NF, Epi EPI>
+__global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restrict__ A, int64_t lda,
+                                                        const uint16_t* __restrict__ B, int64_t ldb,
+                                                        void* __restrict__ C, int64_t ldc, int M,
+                                                        int N, int K, RopeArgs rope) {
+    using R = RowsCfg<MB, NF, EPI>;
+    __shared__ uint4 lds[R::NST * R::STAGE];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = blockIdx.x;
+    int slice[NF];
+#pragma unroll
+    for (int f = 0; f < NF; ++f) slice[f] = rows_slice<NF, EPI>(g, f, rope);
+    const char* b_base = reinterpret_cast<const char*>(B + (int64_t)slice[0] * ldb);
+    const char* a_base = reinterpret_cast<const char*>(A);
+    // Load j of this thread fills slot (wave * LOADS + j) * 64 + lane of a stage: slots
+    // [0, ROWS_B * CH) hold the B slices, the rest the A rows; the chunk order inside a
+    // row is XOR-swizzled with the row's low 4 bits (16 rows read at one logical chunk
+    // hit 16 distinct bank groups).  Offsets are relative to b_base / a_base.
+    uint32_t goff[R::LOADS];
+#pragma unroll
+    for (int j = 0; j < R::LOADS; ++j) {
+        const int slot = (wave * R::LOADS + j) * 64 + lane;
+        if (slot < R::ROWS_B * R::CH) {
+            const int r = slot / R::CH, c = (slot % R::CH) ^ (r & 15);
+            const int row = min(slice[r >> 4] + (r & 15), N - 1) - slice[0];
+            goff[j] = (uint32_t)(((int64_t)row * ldb + c * 8) * 2);
+        } else {
+            const int sa = slot - R::ROWS_B * R::CH;
+            const int r = sa / R::CH, c = (sa % R::CH) ^ (r & 15);
+            goff[j] = (uint32_t)(((int64_t)min(r, M - 1) * lda + c * 8) * 2);
+        }
+    }
+    const uint32_t lds_base = lds_offset(lds);
+    auto issue = [&](int stage, int k0) {
+#pragma unroll
+        for (int j = 0; j < R::LOADS; ++j) {
+            const bool is_b = (wave * R::LOADS + j) * 64 < R::ROWS_B * R::CH;
+            dma_load_16B((is_b ? b_base : a_base) + 2 * (int64_t)k0 + goff[j],
+                         lds_base + (uint32_t)((stage * R::STAGE + (wave * R::LOADS + j) * 64) * 16));
+        }
+    };
+    const int nk = K / R::BK;
+#pragma unroll
+    for (int st = 0; st < R::NST - 1; ++st) issue(st, min(st, nk - 1) * R::BK);
+    f32x4 acc[NF];
+#pragma unroll
+    for (int f = 0; f < NF; ++f) acc[f] = f32x4{};
+    const int rb = lane & 15, ck = lane >> 4;
+    for (int kt = 0; kt < nk; ++kt) {
+        wait_vmcnt<(R::NST - 2) * R::LOADS>();  // this thread's part of stage kt landed
+        __syncthreads();                         // everyone's part; stage kt-1 fully read
+        issue((kt + R::NST - 1) % R::NST, min(kt + R::NST - 1, nk - 1) * R::BK);
+        if (wave < MB) {
+            const uint4* L = lds + (kt % R::NST) * R::STAGE;
+#pragma unroll
+            for (int s = 0; s < R::BK / 32; ++s) {
+                const int c = 4 * s + ck;
+                bf16x8 fw[NF];
+#pragma unroll
+                for (int f = 0; f < NF; ++f) {
+                    const int r = 16 * f + rb;
+                    fw[f] = __builtin_bit_cast(bf16x8, L[r * R::CH + (c ^ (r & 15))]);
+                }
+                const int ra = 16 * wave + rb;
+                const bf16x8 fx = __builtin_bit_cast(bf16x8, L[R::ROWS_B * R::CH + ra * R::CH + (c ^ (ra & 15))]);
+#pragma unroll
+                for (int f = 0; f < NF; ++f)
+                    acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[f], fx, acc[f], 0, 0, 0);
+            }
+        }
+    }
+    wait_vmcnt<0>();  // no DMA may still target LDS when the workgroup retires
+    if (wave >= MB) return;
+
+    // Lane owns row m = 16 wave + (lane & 15) and, per slice f, columns
+    // slice[f] + 4 (lane >> 4) + {0..3} in acc[f][0..3].
+    const int m = 16 * wave + rb;
+    if (m >= M) return;
+    if constexpr (EPI == Epi::SwiGLU) {
+        const int col = 32 * (g >> 1) + 16 * (g & 1) + 4 * ck;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = silu(acc[0][e]) * acc[1][e];
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(C) + (int64_t)m * ldc + col) =
+            make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+    } else if constexpr (EPI == Epi::StoreActRope) {
+        if (slice[0] < rope.cols) {
+            const int hd = rope.head_dim, half = hd >> 1;
+            const int i0 = slice[0] % hd + 4 * ck;  // first-half index of this lane's 4 columns
+            const float4* t = reinterpret_cast<const float4*>(rope.cs + (int64_t)rope.pos[m] * half + i0);
+            const float4 t0 = t[0], t1 = t[1];
+            const float c4[4] = {t0.x, t0.z, t1.x, t1.z};
+            const float s4[4] = {t0.y, t0.w, t1.y, t1.w};
+            float v[4], w[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                v[e] = rope_rot(acc[0][e], acc[1][e], c4[e], s4[e], true);
+                w[e] = rope_rot(acc[1][e], acc[0][e], c4[e], s4[e], false);
+            }
+            uint16_t* out = static_cast<uint16_t*>(C) + (int64_t)m * ldc;
+            *reinterpret_cast<uint2*>(out + slice[0] + 4 * ck) =
+                make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+            *reinterpret_cast<uint2*>(out + slice[1] + 4 * ck) =
+                make_uint2(pack_bf16x2(w[0], w[1]), pack_bf16x2(w[2], w[3]));
+        } else {
+#pragma unroll
+            for (int f = 0; f < NF; ++f) {
+                const int n = slice[f] + 4 * ck;
+                if (rope.vt) {
+                    const int64_t vc = rope.vcol[m];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        rope.vt[(int64_t)(n + e - rope.cols) * rope.ld_vt + vc] = (uint16_t)f32_to_bf16(acc[f][e]);
+                } else {
+                    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
+                        make_uint2(pack_bf16x2(acc[f][0], acc[f][1]), pack_bf16x2(acc[f][2], acc[f][3]));
+                }
+            }
+        }
+    } else {
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            const int n = slice[f] + 4 * ck;
+            if (n >= N) continue;
+            if constexpr (EPI == Epi::StoreAct) {
+                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
+                    make_uint2(pack_bf16x2(acc[f][0], acc[f][1]), pack_bf16x2(acc[f][2], acc[f][3]));
+            } else if constexpr (EPI == Epi::StoreF32) {
+                *reinterpret_cast<f32x4*>(static_cast<float*>(C) + (int64_t)m * ldc + n) = acc[f];
+            } else {
+                f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(C) + (int64_t)m * ldc + n);
+                *p = *p + acc[f];
+            }
+        }
+    }
+}
+
 #ifndef SURR_GEMM_KERNELS_ONLY  // (kernel-only builds for standalone tuning harnesses)
 template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI>
 hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
@@ -380,13 +567,33 @@ hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void
     return hipGetLastError();
 }
 
+template <int MB, Epi EPI>
+hipError_t run_rows(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
+                    int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
+    constexpr int NF = (EPI == Epi::SwiGLU || EPI == Epi::StoreActRope) ? 2 : 1;
+    const unsigned groups = (unsigned)(N / (16 * NF));
+    gemm_rows_kernel<MB, NF, EPI><<<groups, RowsCfg<MB, NF, EPI>::THREADS, 0, s>>>(
+        static_cast<const uint16_t*>(A), lda, static_cast<const uint16_t*>(B), ldb, C, ldc, M, N, K,
+        rope);
+    return hipGetLastError();
+}
+
 // Tile choice (measured on the 7B projection shapes): 256 x 256 x 32 tiles, eight
 // wavefronts of 128 x 64 (two per SIMD, so one hides the other's waits), a 3-stage ring
-// and XCD-grouped order; 128 x 128 tiles for the few-row GEMMs of the last-position
-// head, the pruned final layer and decode steps.
+// and XCD-grouped order; up to 64 rows (decode steps, last-position rows) the few-row
+// kernel; 128 x 128 tiles up to 128 rows.
 template <Epi EPI>
 hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                          int64_t ldc, int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
+    // the few-row kernel needs whole 32-row slice pairs and K in 128-column stages; RoPE
+    // slices pair whole half-heads, so the rotated width and V width split into 32-row groups
+    const bool rows_ok = N % 32 == 0 && K % 128 == 0 &&
+                         (EPI != Epi::StoreActRope || (rope.cols % 32 == 0 && (rope.head_dim >> 1) % 16 == 0));
+    if (M <= 64 && rows_ok) {
+        if (M <= 16) return run_rows<1, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        if (M <= 32) return run_rows<2, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        return run_rows<4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+    }
     if (M <= 128)
         return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
     return run_bf16<256, 256, 32, 128, 64, 3, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
