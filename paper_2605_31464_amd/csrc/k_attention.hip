@@ -370,6 +370,168 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
     for (int d = 0; d < HD; ++d) orow[d] = o[d] * inv;
 }
 
+
+// ---------------------------------------------------------------- one-token continuations
+// A decode step appends one token to each cached sequence; its attention is one query row
+// per head against every key of the entry (the cached ones plus the token's own, which the
+// layer has already appended to the cache).  Walking those keys with a 128-row query tile
+// would serialise thousands of keys in one workgroup, so the keys are cut into kDecKS-key
+// slices instead: workgroup (item, kv head) scores the group's G <= 16 query heads against
+// one slice, forms the slice's softmax statistics (max and sum of exp, fp32) and its
+// unnormalised weighted V sum, and attn_decode_combine_kernel merges the slices of each
+// head in slice order.  Both products run on v_mfma_f32_16x16x32_bf16 with operands read
+// straight from the cache in MFMA layout: S^T = K Q^T (16 keys x 16 heads per block;
+// wavefront w owns keys [64 w, 64 w + 64) of the slice) and O^T = V^T P^T (16 dims x 16
+// heads per block; wavefront w owns HD / 64 blocks of 16 dims), with P in bf16 as in the
+// tiled kernel.  V^T column c of an entry holds key vt_key_order(c), so P^T is staged in
+// LDS in column order and read back as 16-byte B fragments.  Every step runs in a fixed
+// order, so a row's result depends only on its own sequence.
+constexpr int kDecKS = 256, kDecMaxG = 16;
+
+template <int HD>
+__global__ __launch_bounds__(256) void attn_decode_split_kernel(
+    const uint16_t* __restrict__ qkv, int64_t ld_qkv, const int32_t* __restrict__ cu,
+    const int2* __restrict__ items, const int32_t* __restrict__ dprompt, int n_q_heads,
+    int n_kv_heads, float scale, PrefixKV pk, float* __restrict__ part) {
+    constexpr int KS = HD / 32;   // 32-dim steps of the score product
+    constexpr int DB = HD / 64;   // 16-dim blocks of O per wavefront
+    __shared__ __attribute__((aligned(16))) uint16_t pst[16][kDecKS + 8];  // P^T, column order
+    __shared__ float red[2][4][16];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 15, lg = lane >> 4;
+    const int item = blockIdx.x / n_kv_heads, hk = blockIdx.x % n_kv_heads;
+    const int2 it = items[item];
+    const int b = dprompt[it.x];
+    const int G = n_q_heads / n_kv_heads;
+    const int nkeys = pk.len[b] + 1;
+    const int64_t off = pk.off[b];
+    const int k0 = it.y * kDecKS, k1 = min(k0 + kDecKS, nkeys);
+    const int64_t t = cu[b];
+    const uint16_t* K = static_cast<const uint16_t*>(pk.k);
+    const uint16_t* VT = static_cast<const uint16_t*>(pk.v);
+    const uint4 zero = {0, 0, 0, 0};
+
+    // all global loads first: Q fragments (head li), K fragments of this wavefront's 64
+    // keys, V^T fragments of its dims over the slice (rows of keys past k1 are not read)
+    uint4 qf[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+        qf[s] = li < G ? *reinterpret_cast<const uint4*>(qkv + t * ld_qkv + (int64_t)(hk * G + li) * HD + 32 * s + 8 * lg)
+                       : zero;
+    uint4 kf[4][KS];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+        const int key = k0 + 64 * wave + 16 * kb + li;
+        const uint16_t* kr = K + (off + key) * pk.ld_k + (int64_t)hk * HD + 8 * lg;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) kf[kb][s] = key < k1 ? *reinterpret_cast<const uint4*>(kr + 32 * s) : zero;
+    }
+    const int c_end = (k1 + 15) & ~15;  // V^T columns of 16-key groups that hold live keys
+    uint4 vf[DB][kDecKS / 32];
+#pragma unroll
+    for (int d = 0; d < DB; ++d) {
+        const uint16_t* vr = VT + (int64_t)(hk * HD + 16 * (DB * wave + d) + li) * pk.ld_v + off + 8 * lg;
+#pragma unroll
+        for (int s = 0; s < kDecKS / 32; ++s) {
+            const int c = k0 + 32 * s + 8 * lg;
+            vf[d][s] = c < c_end ? *reinterpret_cast<const uint4*>(vr + k0 + 32 * s) : zero;
+        }
+    }
+
+    // S^T = K Q^T: lane holds keys 16 kb + 4 lg + r of its wavefront, head li
+    f32x4 sc[4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+        sc[kb] = f32x4{};
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+            sc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[kb][s]),
+                                                            __builtin_bit_cast(bf16x8, qf[s]), sc[kb], 0, 0, 0);
+    }
+    // softmax statistics per head li over the slice: max, then sum of exp, fixed order
+    float m = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int key = k0 + 64 * wave + 16 * kb + 4 * lg + r;
+            sc[kb][r] = key < k1 ? sc[kb][r] * scale : -INFINITY;
+            m = fmaxf(m, sc[kb][r]);
+        }
+    m = fmaxf(m, __shfl_xor(m, 16, 64));
+    m = fmaxf(m, __shfl_xor(m, 32, 64));
+    if (lg == 0) red[0][wave][li] = m;
+    __syncthreads();
+    m = fmaxf(fmaxf(red[0][0][li], red[0][1][li]), fmaxf(red[0][2][li], red[0][3][li]));
+    float l = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int kl = 64 * wave + 16 * kb + 4 * lg + r;  // key index inside the slice
+            const float pv = k0 + kl < k1 ? expf(sc[kb][r] - m) : 0.f;
+            l += pv;
+            pst[li][vt_key_order(kl)] = (uint16_t)f32_to_bf16(pv);
+        }
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    if (lg == 0) red[1][wave][li] = l;
+    __syncthreads();
+
+    // O^T = V^T P^T over the slice's 8 steps of 32 columns; dims 16 (DB wave + d) + 4 lg + r
+#pragma unroll
+    for (int d = 0; d < DB; ++d) {
+        f32x4 o = f32x4{};
+#pragma unroll
+        for (int s = 0; s < kDecKS / 32; ++s) {
+            const uint4 pf = *reinterpret_cast<const uint4*>(&pst[li][32 * s + 8 * lg]);
+            o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[d][s]),
+                                                       __builtin_bit_cast(bf16x8, pf), o, 0, 0, 0);
+        }
+        if (li < G) {
+            float* pr = part + ((int64_t)item * n_q_heads + hk * G + li) * (HD + 4);
+            *reinterpret_cast<f32x4*>(pr + 16 * (DB * wave + d) + 4 * lg) = o;
+        }
+    }
+    if (wave == 0 && lg == 0 && li < G) {
+        float* pr = part + ((int64_t)item * n_q_heads + hk * G + li) * (HD + 4);
+        pr[HD] = m;
+        pr[HD + 1] = ((red[1][0][li] + red[1][1][li]) + red[1][2][li]) + red[1][3][li];
+    }
+}
+
+// Merge the slices of decode prompt i, query head a: M = max m_s, L = sum l_s e^(m_s - M),
+// O = sum O_s e^(m_s - M) / L, in slice order; bf16 into the token's output row.  A slice
+// record is HD floats of O, then m and l, padded to HD + 4 floats (16-byte aligned).  The
+// slices' statistics are fetched in parallel into LDS first (at most kDecMaxSlices).
+constexpr int kDecMaxSlices = 64;
+
+template <int HD>
+__global__ __launch_bounds__(HD) void attn_decode_combine_kernel(
+    const float* __restrict__ part, const int32_t* __restrict__ dfirst,
+    const int32_t* __restrict__ dprompt, const int32_t* __restrict__ cu, int n_q_heads,
+    uint16_t* __restrict__ out, int64_t ld_out) {
+    __shared__ float ms[kDecMaxSlices], ls[kDecMaxSlices];
+    const int i = blockIdx.x / n_q_heads, a = blockIdx.x % n_q_heads, e = threadIdx.x;
+    const int f0 = dfirst[i], n = dfirst[i + 1] - f0;
+    for (int f = e; f < n; f += HD) {
+        const float* pr = part + ((int64_t)(f0 + f) * n_q_heads + a) * (HD + 4);
+        ms[f] = pr[HD];
+        ls[f] = pr[HD + 1];
+    }
+    __syncthreads();
+    float M = -INFINITY;
+    for (int f = 0; f < n; ++f) M = fmaxf(M, ms[f]);
+    float L = 0.f, o = 0.f;
+#pragma unroll 8
+    for (int f = 0; f < n; ++f) {
+        const float w = expf(ms[f] - M);
+        L = fmaf(ls[f], w, L);
+        o = fmaf(part[((int64_t)(f0 + f) * n_q_heads + a) * (HD + 4) + e], w, o);
+    }
+    out[(int64_t)cu[dprompt[i]] * ld_out + (int64_t)a * HD + e] = (uint16_t)f32_to_bf16(o / L);
+}
+
 }  // namespace
 
 int attention_q_tile(Act t) { return t == Act::BF16 ? kBQ : kBQ32; }
@@ -418,6 +580,39 @@ hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, const void* 
             default: return hipErrorInvalidValue;
         }
 #undef SURR_ATTN_F32
+    }
+    return hipGetLastError();
+}
+
+
+int attention_decode_slice() { return kDecKS; }
+int attention_decode_max_slices() { return kDecMaxSlices; }
+
+hipError_t launch_attention_decode(const void* qkv, int64_t ld_qkv, const int32_t* cu,
+                                   const int2* items, int n_items, const int32_t* dprompt,
+                                   const int32_t* dfirst, int n_prompts, int n_q_heads,
+                                   int n_kv_heads, int head_dim, const PrefixKV& pk, float* part,
+                                   void* out, int64_t ld_out, hipStream_t s) {
+    if (n_items == 0) return hipSuccess;
+    const int G = n_q_heads / n_kv_heads;
+    if (G < 1 || G > kDecMaxG || G * n_kv_heads != n_q_heads || !pk.k || !pk.v || !pk.len ||
+        !pk.off || pk.ld_k % 8 || pk.ld_v % 8)
+        return hipErrorInvalidValue;
+    const float scale = 1.f / sqrtf((float)head_dim);
+    const uint16_t* q = static_cast<const uint16_t*>(qkv);
+    uint16_t* o = static_cast<uint16_t*>(out);
+    const unsigned g1 = (unsigned)n_items * (unsigned)n_kv_heads;
+    const unsigned g2 = (unsigned)n_prompts * (unsigned)n_q_heads;
+    switch (head_dim) {
+        case 64:
+            attn_decode_split_kernel<64><<<g1, 256, 0, s>>>(q, ld_qkv, cu, items, dprompt, n_q_heads, n_kv_heads, scale, pk, part);
+            attn_decode_combine_kernel<64><<<g2, 64, 0, s>>>(part, dfirst, dprompt, cu, n_q_heads, o, ld_out);
+            break;
+        case 128:
+            attn_decode_split_kernel<128><<<g1, 256, 0, s>>>(q, ld_qkv, cu, items, dprompt, n_q_heads, n_kv_heads, scale, pk, part);
+            attn_decode_combine_kernel<128><<<g2, 128, 0, s>>>(part, dfirst, dprompt, cu, n_q_heads, o, ld_out);
+            break;
+        default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }

@@ -302,44 +302,92 @@ __global__ __launch_bounds__(256) void append_vt_kernel(const uint16_t* __restri
     }
 }
 
-// Next-token read-out per row of logits: LSE over the vocabulary (same order of
-// operations as lse_verdict_kernel), the first argmax, and optionally the log-prob of a
-// given target id.
-__global__ __launch_bounds__(256) void lse_next_kernel(const float* __restrict__ logits, int64_t ld,
-                                                       int V, const int32_t* __restrict__ target,
-                                                       int32_t* __restrict__ next_token,
-                                                       float* __restrict__ target_lp) {
-    __shared__ float red[4];
-    __shared__ int redi[4];
+// Full-vocabulary LSE of one row of logits by a workgroup of kLseThreads threads, and
+// optionally its first argmax.  Thread t reads the 16-byte chunks t, t + kLseThreads, ...
+// (each wavefront step covers 1 KB contiguous), so a row streams at full width instead of
+// one value per thread.  Every reduction runs in a fixed order (a thread's values in index
+// order, a butterfly across lanes, then the waves in order), so the result depends on the
+// row alone.  max ignores NaN (fmaxf); the argmax takes the larger value, the lower index
+// on ties.
+constexpr int kLseThreads = 1024, kLseWaves = kLseThreads / 64;
+
+template <bool ARGMAX>
+__device__ __forceinline__ void row_lse(const float* __restrict__ z, int V, float* red, int* redi,
+                                        float& lse, int& argmax) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int b = blockIdx.x;
-    const float* z = logits + (int64_t)b * ld;
+    const int V4 = (V % 4 == 0 && (reinterpret_cast<uintptr_t>(z) & 15) == 0) ? V / 4 : 0;
+    const float4* z4 = reinterpret_cast<const float4*>(z);
     float mx = -INFINITY;
     int am = V;
-    for (int i = tid; i < V; i += 256) {
-        const float v = z[i];
-        if (v > mx) { mx = v; am = i; }
+    auto take = [&](float v, int i) {
+        if constexpr (ARGMAX) {
+            if (v > mx) { mx = v; am = i; }
+        } else {
+            mx = fmaxf(mx, v);
+        }
+    };
+    for (int i = tid; i < V4; i += kLseThreads) {
+        const float4 v = z4[i];
+        take(v.x, 4 * i);
+        take(v.y, 4 * i + 1);
+        take(v.z, 4 * i + 2);
+        take(v.w, 4 * i + 3);
     }
+    for (int i = 4 * V4 + tid; i < V; i += kLseThreads) take(z[i], i);
+    if constexpr (ARGMAX) {
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {  // larger value wins, the lower index on ties
-        const float ov = __shfl_xor(mx, o, 64);
-        const int oi = __shfl_xor(am, o, 64);
-        if (ov > mx || (ov == mx && oi < am)) { mx = ov; am = oi; }
+        for (int o = 32; o > 0; o >>= 1) {
+            const float ov = __shfl_xor(mx, o, 64);
+            const int oi = __shfl_xor(am, o, 64);
+            if (ov > mx || (ov == mx && oi < am)) { mx = ov; am = oi; }
+        }
+    } else {
+        mx = wave_max(mx);
     }
     if (lane == 0) { red[wave] = mx; redi[wave] = am; }
     __syncthreads();
     mx = red[0];
     am = redi[0];
-    for (int w = 1; w < 4; ++w)
-        if (red[w] > mx || (red[w] == mx && redi[w] < am)) { mx = red[w]; am = redi[w]; }
+    for (int w = 1; w < kLseWaves; ++w) {
+        if constexpr (ARGMAX) {
+            if (red[w] > mx || (red[w] == mx && redi[w] < am)) { mx = red[w]; am = redi[w]; }
+        } else {
+            mx = fmaxf(mx, red[w]);
+        }
+    }
     __syncthreads();
-    float s = 0.f;
-    for (int i = tid; i < V; i += 256) s += expf(z[i] - mx);
-    s = wave_sum(s);
-    if (lane == 0) red[wave] = s;
+    float sum = 0.f;
+    for (int i = tid; i < V4; i += kLseThreads) {
+        const float4 v = z4[i];
+        sum += expf(v.x - mx);
+        sum += expf(v.y - mx);
+        sum += expf(v.z - mx);
+        sum += expf(v.w - mx);
+    }
+    for (int i = 4 * V4 + tid; i < V; i += kLseThreads) sum += expf(z[i] - mx);
+    sum = wave_sum(sum);
+    if (lane == 0) red[wave] = sum;
     __syncthreads();
-    if (tid == 0) {
-        const float lse = mx + logf(((red[0] + red[1]) + red[2]) + red[3]);
+    float tot = red[0];
+    for (int w = 1; w < kLseWaves; ++w) tot += red[w];
+    lse = mx + logf(tot);
+    argmax = am;
+}
+
+// Next-token read-out per row of logits: the full-vocabulary LSE (as in
+// lse_verdict_kernel), the first argmax, and optionally the log-prob of a given target id.
+__global__ __launch_bounds__(kLseThreads) void lse_next_kernel(const float* __restrict__ logits, int64_t ld,
+                                                               int V, const int32_t* __restrict__ target,
+                                                               int32_t* __restrict__ next_token,
+                                                               float* __restrict__ target_lp) {
+    __shared__ float red[kLseWaves];
+    __shared__ int redi[kLseWaves];
+    const int b = blockIdx.x;
+    const float* z = logits + (int64_t)b * ld;
+    float lse;
+    int am;
+    row_lse<true>(z, V, red, redi, lse, am);
+    if (threadIdx.x == 0) {
         if (next_token) next_token[b] = am;
         if (target_lp) target_lp[b] = z[target[b]] - lse;
     }
@@ -349,31 +397,21 @@ __global__ __launch_bounds__(256) void lse_next_kernel(const float* __restrict__
 // One workgroup per prompt.  LSE = max + log(sum exp(z - max)) over the full vocabulary
 // (fixed-order reductions), lp_v = z[vid_v] - LSE, then p = softmax(lp), q = max p and
 // the first argmax.
-__global__ __launch_bounds__(256) void lse_verdict_kernel(const float* __restrict__ logits,
-                                                          int64_t ld, int V,
-                                                          const int32_t* __restrict__ vid, int nv,
-                                                          float* __restrict__ lp,
-                                                          float* __restrict__ probs,
-                                                          float* __restrict__ conf,
-                                                          int32_t* __restrict__ verdict) {
-    __shared__ float red[4];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+__global__ __launch_bounds__(kLseThreads) void lse_verdict_kernel(const float* __restrict__ logits,
+                                                                  int64_t ld, int V,
+                                                                  const int32_t* __restrict__ vid, int nv,
+                                                                  float* __restrict__ lp,
+                                                                  float* __restrict__ probs,
+                                                                  float* __restrict__ conf,
+                                                                  int32_t* __restrict__ verdict) {
+    __shared__ float red[kLseWaves];
+    __shared__ int redi[kLseWaves];
     const int b = blockIdx.x;
     const float* z = logits + (int64_t)b * ld;
-    float mx = -INFINITY;
-    for (int i = tid; i < V; i += 256) mx = fmaxf(mx, z[i]);
-    mx = wave_max(mx);
-    if (lane == 0) red[wave] = mx;
-    __syncthreads();
-    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-    __syncthreads();
-    float s = 0.f;
-    for (int i = tid; i < V; i += 256) s += expf(z[i] - mx);
-    s = wave_sum(s);
-    if (lane == 0) red[wave] = s;
-    __syncthreads();
-    if (tid == 0) {
-        const float lse = mx + logf(((red[0] + red[1]) + red[2]) + red[3]);
+    float lse;
+    int am;
+    row_lse<false>(z, V, red, redi, lse, am);
+    if (threadIdx.x == 0) {
         float l[16];
         float m2 = -INFINITY;
         for (int v = 0; v < nv; ++v) {
@@ -657,7 +695,7 @@ hipError_t launch_gather_rows(const void* src, int64_t ld_src, const int32_t* ro
 hipError_t launch_lse_verdict(const float* logits, int64_t ld, int B, int V, const int32_t* vid,
                               int nv, float* lp, float* probs, float* conf, int32_t* verdict,
                               hipStream_t s) {
-    lse_verdict_kernel<<<B, 256, 0, s>>>(logits, ld, V, vid, nv, lp, probs, conf, verdict);
+    lse_verdict_kernel<<<B, kLseThreads, 0, s>>>(logits, ld, V, vid, nv, lp, probs, conf, verdict);
     return hipGetLastError();
 }
 
@@ -683,7 +721,7 @@ hipError_t launch_append_vt(const uint16_t* vt, int64_t ld_vt, const int32_t* vt
 
 hipError_t launch_lse_next(const float* logits, int64_t ld, int B, int V, const int32_t* target,
                            int32_t* next_token, float* target_lp, hipStream_t s) {
-    lse_next_kernel<<<B, 256, 0, s>>>(logits, ld, V, target, next_token, target_lp);
+    lse_next_kernel<<<B, kLseThreads, 0, s>>>(logits, ld, V, target, next_token, target_lp);
     return hipGetLastError();
 }
 

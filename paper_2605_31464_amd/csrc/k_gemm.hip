@@ -380,24 +380,27 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
 // ---------------------------------------------------------------- few-row GEMM
 // C = A[M,K] * B[N,K]^T for M <= 16 MB rows (decode steps, last-position rows).  With so
 // few rows the work is reading B once, so each workgroup streams NF 16-row slices of B
-// over the whole K through a deep LDS ring (direct-to-LDS loads, up to ~60 KB in flight
-// per workgroup), together with the M rows of A; wavefront w < MB multiplies row block w
-// (v_mfma_f32_16x16x32_bf16).  Each output still accumulates k in ascending MFMA steps in
+// over the whole K through a deep LDS ring of BK-column stages (direct-to-LDS loads; the
+// ring holds 128 KB, about half of it B), together with the M rows of A; wavefront w < MB
+// multiplies row block w (v_mfma_f32_16x16x32_bf16).  One barrier per stage: with BK = 256
+// a stage carries 8 dependent MFMA steps, enough to amortise the barrier and the LDS
+// latency (128-column stages halve that and run about half as fast).  Each output still accumulates k in ascending MFMA steps in
 // one fp32 accumulator, as in the tiled kernel (whose 32x32x16 steps give bitwise the same
 // sums), so a row's result does not depend on how many rows share the call.
 // The NF slices of workgroup g: plain epilogues one slice, rows [16 g, 16 g + 16); SwiGLU a
 // gate slice and its up slice 32 rows further (gate/up rows interleave in 32-row blocks);
 // RoPE a slice of the first half of a head and its partner half a head further, and, past
 // the rotated columns, two consecutive slices of V columns.
-template <int MB, int NF, Epi EPI>
+template <int MB, int NF, Epi EPI, int BK_ = 256>
 struct RowsCfg {
-    static constexpr int BK = 128, CH = BK / 8;          // 16-byte chunks per row and stage
+    static constexpr int BK = BK_, CH = BK / 8;          // 16-byte chunks per row and stage
     static constexpr int ROWS_B = 16 * NF, ROWS_A = 16 * MB;
     static constexpr int STAGE = (ROWS_B + ROWS_A) * CH;  // 16-byte slots per stage
     static constexpr int THREADS = 256;
     static constexpr int LOADS = STAGE / THREADS;
     static constexpr int NST0 = 8192 / STAGE;             // 128 KB of ring
     static constexpr int NST = NST0 > 16 ? 16 : NST0;
+    static_assert(CH >= 16, "swizzle with the row's low 4 bits");
     static_assert(STAGE % THREADS == 0 && (ROWS_B * CH) % 64 == 0, "whole wavefront loads");
     static_assert(NST >= 3 && (NST - 2) * LOADS <= 63, "ring depth");
     static_assert(MB <= 4, "one row block per wavefront");
@@ -419,12 +422,12 @@ __device__ __forceinline__ int rows_slice(int g, int f, const RopeArgs& rope) {
     }
 }
 
-template <int MB, int NF, Epi EPI>
+template <int MB, int NF, Epi EPI, int BK>
 __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restrict__ A, int64_t lda,
                                                         const uint16_t* __restrict__ B, int64_t ldb,
                                                         void* __restrict__ C, int64_t ldc, int M,
                                                         int N, int K, RopeArgs rope) {
-    using R = RowsCfg<MB, NF, EPI>;
+    using R = RowsCfg<MB, NF, EPI, BK>;
     __shared__ uint4 lds[R::NST * R::STAGE];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = blockIdx.x;
@@ -572,9 +575,17 @@ hipError_t run_rows(const void* A, int64_t lda, const void* B, int64_t ldb, void
                     int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
     constexpr int NF = (EPI == Epi::SwiGLU || EPI == Epi::StoreActRope) ? 2 : 1;
     const unsigned groups = (unsigned)(N / (16 * NF));
-    gemm_rows_kernel<MB, NF, EPI><<<groups, RowsCfg<MB, NF, EPI>::THREADS, 0, s>>>(
-        static_cast<const uint16_t*>(A), lda, static_cast<const uint16_t*>(B), ldb, C, ldc, M, N, K,
-        rope);
+    const uint16_t* a = static_cast<const uint16_t*>(A);
+    const uint16_t* b = static_cast<const uint16_t*>(B);
+    if constexpr (MB + NF <= 4) {  // 256-column stages while the ring keeps >= 4 of them
+        if (K % 256 == 0) {
+            gemm_rows_kernel<MB, NF, EPI, 256><<<groups, RowsCfg<MB, NF, EPI, 256>::THREADS, 0, s>>>(
+                a, lda, b, ldb, C, ldc, M, N, K, rope);
+            return hipGetLastError();
+        }
+    }
+    gemm_rows_kernel<MB, NF, EPI, 128><<<groups, RowsCfg<MB, NF, EPI, 128>::THREADS, 0, s>>>(
+        a, lda, b, ldb, C, ldc, M, N, K, rope);
     return hipGetLastError();
 }
 

@@ -171,4 +171,17 @@ hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, const void* 
                             int head_dim, hipStream_t s, const PrefixKV* pf = nullptr);
 int attention_q_tile(Act t);
 
+// One-token continuations of cached sequences (bf16): for decode prompt i = items[n].x
+// (prompt dprompt[i], whose only row is cu[b] and whose entry holds pk.len[b] + 1 keys
+// once this layer's key is appended), slice items[n].y covers keys
+// [y * attention_decode_slice(), +slice).  Items of prompt i are dfirst[i] .. dfirst[i+1]-1.
+// part holds n_items * n_q_heads * (head_dim + 4) floats; the merged rows go to out.
+int attention_decode_slice();
+int attention_decode_max_slices();  // per prompt
+hipError_t launch_attention_decode(const void* qkv, int64_t ld_qkv, const int32_t* cu,
+                                   const int2* items, int n_items, const int32_t* dprompt,
+                                   const int32_t* dfirst, int n_prompts, int n_q_heads,
+                                   int n_kv_heads, int head_dim, const PrefixKV& pk, float* part,
+                                   void* out, int64_t ld_out, hipStream_t s);
+
 }  // namespace surr

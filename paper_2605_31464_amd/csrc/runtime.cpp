@@ -47,8 +47,10 @@ struct LayerW {
 
 // Byte offsets of one call's workspace regions.
 struct WsLayout {
-    size_t cu, last, vid, work, work_last, vt_off, pfx_len, pfx_off, target, pos, vcol, x, h, qkv, vt, o,
-        u, gu, o_last, x_last, h_last, u_last, gu_last, y, logits, total;
+    size_t cu, last, vid, work, work_last, vt_off, pfx_len, pfx_off, target, dec_items, dec_first,
+        dec_prompt, pos, vcol, x, h, qkv, vt, o, u, gu, o_last, x_last, h_last, u_last, gu_last, y,
+        logits, dec_part, total;
+    int64_t dec_cap;  // decode-attention slice items the workspace holds (bf16 models)
     int64_t ld_vt;  // columns of the transposed V copy (bf16 models)
 };
 
@@ -157,6 +159,11 @@ WsLayout layout(const surrogate_model* m, int64_t B, int64_t T) {
     w.pfx_len = take(4 * B);
     w.pfx_off = take(4 * B);
     w.target = take(4 * B);
+    // one-token continuations: up to ceil(max_pos / slice) key slices per prompt
+    w.dec_cap = f32 ? 0 : B * ((c.max_pos + surr::attention_decode_slice() - 1) / surr::attention_decode_slice());
+    w.dec_items = take(8 * w.dec_cap);
+    w.dec_first = take(4 * (B + 1));
+    w.dec_prompt = take(4 * B);
     w.pos = take(4 * T);
     // Transposed V copy: every prompt's keys start on a 64-column boundary, so its
     // padded ranges need at most T + 63 B columns.
@@ -176,6 +183,7 @@ WsLayout layout(const surrogate_model* m, int64_t B, int64_t T) {
     w.gu_last = f32 ? take(4 * B * 2 * c.d_ff) : 0;
     w.y = take(e * B * c.d_model);
     w.logits = take(4 * B * c.vocab);
+    w.dec_part = take(4 * (size_t)w.dec_cap * c.n_q_heads * (c.head_dim + 4));
     w.total = off;
     return w;
 }
@@ -275,10 +283,26 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
     }
     std::vector<int32_t> vt_off(batch + 1, 0);
     for (int b = 0; b < batch; ++b) vt_off[b + 1] = vt_off[b] + (lengths_h[b] + 63) / 64 * 64;
-    std::vector<int2> work, work_last(batch);
+    // One-token continuations of cached sequences (decode steps) take the split-key decode
+    // attention; every other prompt takes the tiled kernel.  The choice depends on the
+    // prompt alone, so a row's result does not depend on the batch.
+    const bool dec_path = m->act == Act::BF16 && io.append && c.n_q_heads / c.n_kv_heads <= 16 &&
+                          (c.max_pos + surr::attention_decode_slice() - 1) / surr::attention_decode_slice() <=
+                              surr::attention_decode_max_slices();
+    std::vector<int32_t> dprompt, dfirst(1, 0);
+    std::vector<int2> ditems;
+    std::vector<int2> work, work_last;
     for (int b = 0; b < batch; ++b) {
+        if (dec_path && lengths_h[b] == 1) {
+            const int ks = surr::attention_decode_slice();
+            const int ns = (plen[b] + 1 + ks - 1) / ks;
+            for (int s2 = 0; s2 < ns; ++s2) ditems.push_back(make_int2((int)dprompt.size(), s2));
+            dprompt.push_back(b);
+            dfirst.push_back((int32_t)ditems.size());
+            continue;
+        }
         for (int t = 0; t * qt < lengths_h[b]; ++t) work.push_back(make_int2(b, t));
-        work_last[b] = make_int2(b, (lengths_h[b] - 1) / qt);
+        work_last.push_back(make_int2(b, (lengths_h[b] - 1) / qt));
     }
     // Longest key range first (a cached prefix counts in whole tiles), so the big causal
     // tiles start early; stable for a deterministic order.
@@ -311,6 +335,11 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
         std::memcpy(P + w.pfx_len, plen.data(), 4 * plen.size());
         std::memcpy(P + w.pfx_off, poff.data(), 4 * poff.size());
         if (io.target_ids_h) std::memcpy(P + w.target, io.target_ids_h, 4 * (size_t)batch);
+        if (!dprompt.empty()) {
+            std::memcpy(P + w.dec_items, ditems.data(), 8 * ditems.size());
+            std::memcpy(P + w.dec_first, dfirst.data(), 4 * dfirst.size());
+            std::memcpy(P + w.dec_prompt, dprompt.data(), 4 * dprompt.size());
+        }
         SURR_HIP(hipMemcpyAsync(workspace_d, P, meta_bytes, hipMemcpyHostToDevice, stream));
         SURR_HIP(hipEventRecord(m->staged, stream));
         m->staged_pending = true;
@@ -322,6 +351,10 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
     const int32_t* d_vid = reinterpret_cast<const int32_t*>(W + w.vid);
     const int2* d_work = reinterpret_cast<const int2*>(W + w.work);
     const int2* d_work_last = reinterpret_cast<const int2*>(W + w.work_last);
+    const int2* d_dec_items = reinterpret_cast<const int2*>(W + w.dec_items);
+    const int32_t* d_dec_first = reinterpret_cast<const int32_t*>(W + w.dec_first);
+    const int32_t* d_dec_prompt = reinterpret_cast<const int32_t*>(W + w.dec_prompt);
+    float* d_dec_part = reinterpret_cast<float*>(W + w.dec_part);
     int32_t* d_pos = reinterpret_cast<int32_t*>(W + w.pos);
     const int32_t* d_po = reinterpret_cast<const int32_t*>(W + w.vt_off);  // 64-aligned row blocks
     const int32_t* d_pfx_len = reinterpret_cast<const int32_t*>(W + w.pfx_len);
@@ -443,6 +476,8 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
         }
         if (!final_layer) {
             SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, vt, w.ld_vt, d_vt_off, o, dq, d_cu, d_work, (int)work.size(), nq, nkv, hd, stream, pkp));
+            if (!dprompt.empty())
+                SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention_decode(qkv, dqkv, d_cu, d_dec_items, (int)ditems.size(), d_dec_prompt, d_dec_first, (int)dprompt.size(), nq, nkv, hd, pk, d_dec_part, o, dq, stream));
             SURR_PHASE_RUN(SURR_PHASE_GEMM_O, surr::launch_gemm(a, Epi::ResidAddF32, o, dq, L.w_o, dq, x, d, Ti, d, dq, stream));
             SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x, d, nullptr, T, L.mlp_norm, d, c.rms_eps, h, d, stream));
             const surrogate_status st = mlp(L, h, u, gu, x, Ti, SURR_PHASE_GEMM_GATE_UP, SURR_PHASE_GEMM_DOWN);
@@ -450,7 +485,9 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
         } else {
             // Only the last position of each prompt feeds the LM head: K/V above cover
             // every token; attention, O projection and MLP run for the last rows only.
-            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, vt, w.ld_vt, d_vt_off, o, dq, d_cu, d_work_last, batch, nq, nkv, hd, stream, pkp));
+            SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, vt, w.ld_vt, d_vt_off, o, dq, d_cu, d_work_last, (int)work_last.size(), nq, nkv, hd, stream, pkp));
+            if (!dprompt.empty())
+                SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention_decode(qkv, dqkv, d_cu, d_dec_items, (int)ditems.size(), d_dec_prompt, d_dec_first, (int)dprompt.size(), nq, nkv, hd, pk, d_dec_part, o, dq, stream));
             SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gather_rows(o, dq, d_last, batch, dq, (int)m->esz, o_last, dq, stream));
             SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gather_rows(x, d, d_last, batch, d, 4, x_last, d, stream));
             SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_gemm(a, Epi::ResidAddF32, o_last, dq, L.w_o, dq, x_last, d, batch, d, dq, stream));
