@@ -592,7 +592,8 @@ hipError_t run_rows(const void* A, int64_t lda, const void* B, int64_t ldb, void
 // Tile choice (measured on the 7B projection shapes): 256 x 256 x 32 tiles, eight
 // wavefronts of 128 x 64 (two per SIMD, so one hides the other's waits), a 3-stage ring
 // and XCD-grouped order; up to 64 rows (decode steps, last-position rows) the few-row
-// kernel; 128 x 128 tiles up to 128 rows.
+// kernel, up to 128 rows the few-row kernel per 64 rows unless B is wide enough to keep
+// the chip busy with 128 x 128 tiles.
 template <Epi EPI>
 hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                          int64_t ldc, int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
@@ -604,6 +605,24 @@ hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
         if (M <= 16) return run_rows<1, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
         if (M <= 32) return run_rows<2, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
         return run_rows<4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+    }
+    // 65..128 rows against a narrow B: 128 x 128 tiles would leave most CUs idle (N / 128
+    // workgroups), so the few-row kernel runs once per 64 rows, streaming B twice
+    if (M <= 128 && N < 65536 && rows_ok) {
+        constexpr int esz = (EPI == Epi::StoreF32 || EPI == Epi::ResidAddF32) ? 4 : 2;
+        for (int r0 = 0; r0 < M; r0 += 64) {
+            RopeArgs rp = rope;
+            if (rp.pos) rp.pos += r0;
+            if (rp.vcol) rp.vcol += r0;
+            const int mr = min(64, M - r0);
+            const void* a = static_cast<const uint16_t*>(A) + (int64_t)r0 * lda;
+            void* c = static_cast<char*>(C) + (int64_t)r0 * ldc * esz;
+            const hipError_t e = mr <= 16   ? run_rows<1, EPI>(a, lda, B, ldb, c, ldc, mr, N, K, s, rp)
+                                 : mr <= 32 ? run_rows<2, EPI>(a, lda, B, ldb, c, ldc, mr, N, K, s, rp)
+                                            : run_rows<4, EPI>(a, lda, B, ldb, c, ldc, mr, N, K, s, rp);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
     }
     if (M <= 128)
         return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
