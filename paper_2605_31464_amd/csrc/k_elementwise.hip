@@ -113,8 +113,10 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
 
 // Single-pass form for rows of at most 256 * NC values: lane l keeps the float4 chunks
 // l, l + 64, ... of its row in registers, so x is read from HBM exactly once.  Same
-// arithmetic and reduction order as the two-pass kernel above.
-template <bool OUT_BF16, int NC>
+// arithmetic and reduction order as the two-pass kernel above.  With PRE_G the gains are
+// loaded together with x (one memory round trip instead of two; used for the few-row
+// calls of decode steps, where latency, not bandwidth, sets the time).
+template <bool OUT_BF16, int NC, bool PRE_G = false>
 __global__ __launch_bounds__(256) void rmsnorm_reg_kernel(const float* __restrict__ x,
                                                           int64_t ldx,
                                                           const int32_t* __restrict__ rows,
@@ -130,11 +132,16 @@ __global__ __launch_bounds__(256) void rmsnorm_reg_kernel(const float* __restric
     const float4* g4 = reinterpret_cast<const float4*>(g);
     const int n4 = d / 4;
     float4 v[NC];
+    float4 gw[PRE_G ? NC : 1];
 #pragma unroll
     for (int k = 0; k < NC; ++k) {
         const int c = lane + 64 * k;
         v[k] = make_float4(0.f, 0.f, 0.f, 0.f);
         if (c < n4) v[k] = xr[c];
+        if constexpr (PRE_G) {
+            gw[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (c < n4) gw[k] = g4[c];
+        }
     }
     float ss = 0.f;
 #pragma unroll
@@ -146,7 +153,9 @@ __global__ __launch_bounds__(256) void rmsnorm_reg_kernel(const float* __restric
     for (int k = 0; k < NC; ++k) {
         const int c = lane + 64 * k;
         if (c >= n4) continue;
-        const float4 w = g4[c];
+        float4 w;
+        if constexpr (PRE_G) w = gw[k];
+        else w = g4[c];
         const float a = v[k].x * sc * w.x, b = v[k].y * sc * w.y, e = v[k].z * sc * w.z,
                     f = v[k].w * sc * w.w;
         if constexpr (OUT_BF16) {
@@ -167,7 +176,12 @@ hipError_t rmsnorm_dispatch(const float* x, int64_t ldx, const int32_t* rows, in
     const unsigned grid = (unsigned)((n_rows + 3) / 4);
     const int nc = (d / 4 + 63) / 64;
 #define SURR_RMS_REG(NC_)                                                                        \
-    rmsnorm_reg_kernel<OUT_BF16, NC_><<<grid, 256, 0, s>>>(x, ldx, rows, n_rows, g, d, eps, y, ldy)
+    do {                                                                                         \
+        if (n_rows <= 256)                                                                       \
+            rmsnorm_reg_kernel<OUT_BF16, NC_, true><<<grid, 256, 0, s>>>(x, ldx, rows, n_rows, g, d, eps, y, ldy); \
+        else                                                                                     \
+            rmsnorm_reg_kernel<OUT_BF16, NC_><<<grid, 256, 0, s>>>(x, ldx, rows, n_rows, g, d, eps, y, ldy); \
+    } while (0)
     if (nc <= 2) SURR_RMS_REG(2);
     else if (nc <= 4) SURR_RMS_REG(4);
     else if (nc <= 8) SURR_RMS_REG(8);

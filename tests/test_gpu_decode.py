@@ -143,3 +143,46 @@ def test_cache_argument_errors_and_reset():
     assert B.surrogate_cache_lengths(cache, 2).tolist() == [0, 0]
     with pytest.raises(B.SurrogateError):
         B.surrogate_cache_create(scorer.model, [shape.max_pos + 1])
+
+
+def test_decode_entries_crossing_key_slices_match_oracle():
+    """Decode steps of entries whose keys cross the 256-key slices of the decode
+    attention (and end inside partly filled 16-key groups) against the oracle."""
+    shape = synth.CONFIGS["1p5b"].shape.replace(n_layers=2)
+    scorer, W = make_scorer(shape, gain_std=0.1)
+    teacher_forced(scorer, W, shape, [250, 509, 1020], 9, seed=77, tol=TOL["bf16"])
+
+
+def test_row_count_regimes_give_bitwise_equal_rows():
+    """The projections pick a kernel by row count (few-row kernel up to 64 rows, per 64
+    rows up to 128 against narrow weights, tiles above); every choice accumulates in the
+    same order, so a decode step's results do not depend on how many entries share it."""
+    shape = synth.CONFIGS["small"].shape.replace(n_layers=2)
+    scorer, W = make_scorer(shape, gain_std=0.1)
+    n = 140
+    seqs = rng_prompts(shape.vocab, [3 + i % 5 for i in range(n)], 95)
+    tgt = [(7 * i) % shape.vocab for i in range(n)]
+    step = np.array([[11 + i % 13] for i in range(n)], np.int32)
+
+    def run(group):
+        cache = scorer.create_cache([64] * n)
+        for g0 in range(0, n, 70):  # prefill in two calls of 70 (per-64-row regime)
+            ids = list(range(g0, min(n, g0 + 70)))
+            tok, L = padded([seqs[i] for i in ids])
+            scorer.extend(cache, ids, tok, L)
+        lp = np.empty(n, np.float32)
+        nt = np.empty(n, np.int32)
+        for g0 in range(0, n, group):
+            ids = list(range(g0, min(n, g0 + group)))
+            nxt, l = scorer.extend(cache, ids, step[ids], np.ones(len(ids), np.int32),
+                                   [tgt[i] for i in ids])
+            lp[ids] = l.cpu().numpy()
+            nt[ids] = nxt.cpu().numpy()
+        return lp, nt
+
+    ref_lp, ref_nt = run(n)  # 140 rows: tiled projections
+    for group in (1, 13, 30, 64, 100):
+        lp, nt = run(group)
+        assert np.array_equal(lp, ref_lp), group
+        assert np.array_equal(nt, ref_nt), group
+    assert B.surrogate_device_status(scorer.model) == B.SURR_OK
