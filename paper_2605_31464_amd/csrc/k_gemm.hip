@@ -1,29 +1,31 @@
 // Projection GEMMs C = A[M,K] * B[N,K]^T with fused epilogues.
 //
-// bf16 path: v_mfma_f32_32x32x16_bf16 on a BM x BN workgroup tile (4 wavefronts, each
-// WM x WN), K in steps of BK.  Both operands are K-contiguous, so one 16-byte chunk of
+// bf16 path: v_mfma_f32_32x32x16_bf16 or v_mfma_f32_16x16x32_bf16 (MF = 32 or 16) on a
+// BM x BN workgroup tile of WM x WN wavefront tiles, K in steps of BK.  Both MFMA shapes
+// accumulate k in the same order and give bitwise the same sums.  Both operands are K-contiguous, so one 16-byte chunk of
 // a row is exactly the 8 consecutive k values an MFMA lane supplies.  Tiles move from
 // HBM straight into LDS with global_load_lds_dwordx4 (no staging registers) through an
 // NST-stage ring, one barrier per K step; LDS rows hold BK/8 chunks whose order is
 // XOR-swizzled by the row to spread the 16-byte reads over the banks.  The MFMA is issued with the weight fragment as its A operand and the
 // activation fragment as its B operand, so each lane ends up owning one output row m
-// and runs of 4 consecutive output columns n - the shape the epilogues want (8- or
-// 16-byte stores, gate/up pairs and residual rows in one lane).
+// and runs of 4 consecutive output columns n.
 //
 // fp32 path: a plain LDS-tiled FMA kernel for the float32 model.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace surr {
 namespace gemm {
 
-template <int BM, int BN, int BK, int WM, int WN, int NST>
+template <int BM, int BN, int BK, int WM, int WN, int NST, int MF = 32>
 struct Tile {
     static constexpr int WAVES_N = BN / WN;
     static constexpr int NW = (BM / WM) * (BN / WN);  // wavefronts per workgroup
     static constexpr int THREADS = 64 * NW;
     static_assert(NW == 4 || NW == 8 || NW == 16, "4, 8 or 16 wavefronts per workgroup");
-    static constexpr int FM = WM / 32, FN = WN / 32;
+    static constexpr int FM = WM / MF, FN = WN / MF;  // MFMA fragments per wavefront tile
     static constexpr int CH = BK / 8;               // 16-byte chunks per tile row
     static constexpr int A_SLOTS = BM * CH, B_SLOTS = BN * CH;
     static constexpr int STAGE = A_SLOTS + B_SLOTS;  // 16-byte LDS slots per stage
@@ -42,6 +44,14 @@ __device__ __forceinline__ int swz(int row) {
 }
 
 __device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); }
+
+// One MFMA step on a 32x32 (16 fp32 per lane) or 16x16 (4 per lane) accumulator.
+__device__ __forceinline__ f32x16 mfma_step(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_step(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
 
 // Rotate-half RoPE of one value x with its partner y (the value half a head away) and
 // the angle's cos c and sin s: first half x c - y s, second half x c + y s.  Written
@@ -70,14 +80,15 @@ __device__ __forceinline__ void tile_coords(int pid, int tiles_m, int tiles_n, i
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI, int GROUP = 8, bool XCD = false,
-          int SWZ = 0, int MINB = 1>
+          int SWZ = 0, int MINB = 1, int MF = 32>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_kernel(const uint16_t* __restrict__ A,
                                                         int64_t lda,
                                                         const uint16_t* __restrict__ B,
                                                         int64_t ldb, void* __restrict__ C,
                                                         int64_t ldc, int M, int N, int K,
                                                         RopeArgs rope) {
-    using S = Tile<BM, BN, BK, WM, WN, NST>;
+    using S = Tile<BM, BN, BK, WM, WN, NST, MF>;
+    using Acc = typename std::conditional<MF == 32, f32x16, f32x4>::type;
     __shared__ uint4 lds[NST * S::STAGE];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / S::WAVES_N, wn = wave % S::WAVES_N;
@@ -122,26 +133,28 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
                                                                 (wave * S::LOADS + j) * 64) * 16)); \
     } while (0)
 
-    f32x16 acc[S::FM][S::FN];
+    Acc acc[S::FM][S::FN];
 #pragma unroll
     for (int i = 0; i < S::FM; ++i)
 #pragma unroll
-        for (int j = 0; j < S::FN; ++j) acc[i][j] = f32x16{};
+        for (int j = 0; j < S::FN; ++j) acc[i][j] = Acc{};
 
-    // Fragment reads for MFMA step s of the stage at L.
+    // Fragment reads for MFMA step s of the stage at L: lane l supplies row l % MF of the
+    // fragment and its 16-byte chunk l / MF of the step's MFMA_K columns.
+    constexpr int MFMA_K = MF == 32 ? 16 : 32;
     auto read_a = [&](const uint4* L, int s, bf16x8 (&af)[S::FM]) {
-        const int chunk = 2 * s + (lane >> 5);
+        const int chunk = (MFMA_K / 8) * s + lane / MF;
 #pragma unroll
         for (int i = 0; i < S::FM; ++i) {
-            const int r = wm * WM + i * 32 + (lane & 31);
+            const int r = wm * WM + i * MF + lane % MF;
             af[i] = __builtin_bit_cast(bf16x8, L[r * S::CH + (chunk ^ swz<S::CH, SWZ>(r))]);
         }
     };
     auto read_b = [&](const uint4* L, int s, bf16x8 (&bw)[S::FN]) {
-        const int chunk = 2 * s + (lane >> 5);
+        const int chunk = (MFMA_K / 8) * s + lane / MF;
 #pragma unroll
         for (int j = 0; j < S::FN; ++j) {
-            const int r = wn * WN + j * 32 + (lane & 31);
+            const int r = wn * WN + j * MF + lane % MF;
             bw[j] = __builtin_bit_cast(bf16x8, L[S::A_SLOTS + r * S::CH + (chunk ^ swz<S::CH, SWZ>(r))]);
         }
     };
@@ -149,19 +162,21 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
 #define SURR_MFMA_ROWS(cb, i0, i1)                                                            \
     _Pragma("unroll") for (int mi_ = (i0); mi_ < (i1); ++mi_)                                 \
         _Pragma("unroll") for (int mj_ = 0; mj_ < S::FN; ++mj_)                               \
-            acc[mi_][mj_] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cb][mj_], fa[cb][mi_], \
-                                                                    acc[mi_][mj_], 0, 0, 0)
+            acc[mi_][mj_] = mfma_step(fb[cb][mj_], fa[cb][mi_], acc[mi_][mj_])
 
-    // Software pipeline.  Stage ring of NST buffers; the fragments of MFMA step s+1 are
-    // read while the MFMAs of step s run.  With NST >= 3, the DMA of stage kt+NST-1 is
-    // spread between the MFMAs of the first step of stage kt (its buffer was released by
-    // the barrier that opened stage kt), keeping NST-1 stages in flight without stalling
-    // MFMA issue.  With NST == 2 the refill has to wait for that barrier instead.  The
-    // last step of a stage waits for the next stage (vmcnt), passes the barrier and reads
-    // the next stage's first fragments.  sched_barrier pins this order.
-    constexpr int KSTEPS = BK / 16;
+    // Software pipeline.  Stage ring of NST >= 3 buffers; the fragments of MFMA step s+1
+    // are read while the MFMAs of step s run.  The DMA of stage kt+NST-1 is spread between
+    // the MFMA rows of the first step of stage kt (its buffer was released by the barrier
+    // that opened stage kt), keeping NST-1 stages in flight without stalling MFMA issue.
+    // The last step of a stage runs half its MFMA rows, waits for the next stage (vmcnt),
+    // passes the barrier, reads the next stage's first fragments and runs the other half.
+    // With one MFMA step per stage (16x16x32 at BK = 32) the refill goes between the rows
+    // of that half, and the fragment buffers alternate between stages (the stage loop is
+    // unrolled by two).  sched_barrier pins this order.
+    constexpr int KSTEPS = BK / MFMA_K;
     constexpr int FH = S::FM / 2;
-    static_assert(KSTEPS % 2 == 0 && S::FM % 2 == 0, "fragment double buffer");
+    static_assert(NST >= 3, "ring of at least three stages");
+    static_assert((KSTEPS == 1 || KSTEPS % 2 == 0) && S::FM % 2 == 0, "fragment double buffer");
     const int nk = K / BK;
     // Stage loads past the end of K re-load the last stage (always in bounds) into a
     // buffer that is never read again; this keeps the loop free of branches, which the
@@ -170,47 +185,50 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     for (int st = 0; st < NST - 1; ++st) SURR_ISSUE_STAGE(st, min(st, nk - 1) * BK);
     wait_vmcnt<(NST - 2) * S::LOADS>();
     __syncthreads();
-    if (NST == 2) SURR_ISSUE_STAGE(1, min(1, nk - 1) * BK);
     bf16x8 fa[2][S::FM], fb[2][S::FN];
     read_a(lds, 0, fa[0]);
     read_b(lds, 0, fb[0]);
 
-    for (int kt = 0; kt < nk; ++kt) {
+    // refill loads [row * LOADS / ROWS, (row + 1) * LOADS / ROWS) after MFMA row `row`
+#define SURR_REFILL_AFTER_ROWS(cb, rows_, rs_, rk_)                                                     \
+    _Pragma("unroll") for (int row = 0; row < (rows_); ++row) {                                         \
+        SURR_MFMA_ROWS(cb, row, row + 1);                                                               \
+        __builtin_amdgcn_sched_barrier(0);                                                              \
+        _Pragma("unroll") for (int jj = row * S::LOADS / (rows_); jj < (row + 1) * S::LOADS / (rows_); ++jj) \
+            dma_load_16B(SURR_DMA_SRC(jj, rk_),                                                         \
+                         lds_base + (uint32_t)(((rs_) * S::STAGE + (wave * S::LOADS + jj) * 64) * 16)); \
+        __builtin_amdgcn_sched_barrier(0);                                                              \
+    }
+
+    auto stage_fn = [&](int kt, auto cb0_c) {
+        constexpr int CB0 = decltype(cb0_c)::value;
         const uint4* L = lds + (kt % NST) * S::STAGE;
+        const int rs = (kt + NST - 1) % NST, rk = min(kt + NST - 1, nk - 1) * BK;
 #pragma unroll
         for (int s = 0; s < KSTEPS; ++s) {
-            const int cb = s & 1;
+            const int cb = (s + CB0) & 1;
             if (s + 1 < KSTEPS) {
                 read_b(L, s + 1, fb[cb ^ 1]);
                 read_a(L, s + 1, fa[cb ^ 1]);
                 __builtin_amdgcn_sched_barrier(0);
-                if (NST >= 3 && s == 0) {
-                    const int rs = (kt + NST - 1) % NST, rk = min(kt + NST - 1, nk - 1) * BK;
-#pragma unroll
-                    for (int row = 0; row < S::FM; ++row) {
-                        SURR_MFMA_ROWS(cb, row, row + 1);
-                        __builtin_amdgcn_sched_barrier(0);
-                        // loads [row * LOADS / FM, (row + 1) * LOADS / FM) after MFMA row `row`
-#pragma unroll
-                        for (int jj = row * S::LOADS / S::FM; jj < (row + 1) * S::LOADS / S::FM; ++jj) {
-                            dma_load_16B(SURR_DMA_SRC(jj, rk),
-                                         lds_base + (uint32_t)((rs * S::STAGE + (wave * S::LOADS + jj) * 64) * 16));
-                        }
-                        __builtin_amdgcn_sched_barrier(0);
-                    }
+                if (s == 0) {
+                    SURR_REFILL_AFTER_ROWS(cb, S::FM, rs, rk);
                 } else {
                     SURR_MFMA_ROWS(cb, 0, S::FM);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             } else {
-                SURR_MFMA_ROWS(cb, 0, FH);
+                if (KSTEPS == 1) {
+                    SURR_REFILL_AFTER_ROWS(cb, FH, rs, rk);
+                } else {
+                    SURR_MFMA_ROWS(cb, 0, FH);
+                }
                 __builtin_amdgcn_sched_barrier(0);
                 // every wave's reads of stage kt are done before anyone refills it; then
                 // stage kt+1 (issued NST-1 stages ago) must have landed
                 __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));  // lgkmcnt(0)
                 wait_vmcnt<(NST - 2) * S::LOADS>();
                 __syncthreads();
-                if (NST == 2) SURR_ISSUE_STAGE(kt % 2, min(kt + 2, nk - 1) * BK);
                 const uint4* Ln = lds + ((kt + 1) % NST) * S::STAGE;
                 read_a(Ln, 0, fa[cb ^ 1]);
                 read_b(Ln, 0, fb[cb ^ 1]);
@@ -219,21 +237,37 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
+    };
+    if constexpr (KSTEPS % 2 == 0) {
+        for (int kt = 0; kt < nk; ++kt) stage_fn(kt, std::integral_constant<int, 0>());
+    } else {
+        int kt = 0;
+        for (; kt + 1 < nk; kt += 2) {
+            stage_fn(kt, std::integral_constant<int, 0>());
+            stage_fn(kt + 1, std::integral_constant<int, 1>());
+        }
+        if (kt < nk) stage_fn(kt, std::integral_constant<int, 0>());
     }
+#undef SURR_REFILL_AFTER_ROWS
     wait_vmcnt<0>();  // no DMA may still target LDS when the workgroup retires
 #undef SURR_MFMA_ROWS
 
 #undef SURR_ISSUE_STAGE
 #undef SURR_DMA_SRC
 
-    // Lane owns row m = m0 + wm*WM + 32 i + (lane & 31) and, per 32-column fragment j,
-    // columns nb + 8 q + 4 (lane >> 5) + {0..3} in acc[i][j][4 q + {0..3}].
-    const int h = lane >> 5;
+    // Lane owns row m = m0 + wm*WM + MF i + lane % MF and, per fragment j, groups of 4
+    // consecutive columns: with MF = 32 the columns j*32 + 8 q + 4 (lane / 32) + {0..3} in
+    // acc[i][j][4 q + {0..3}] (q < 4); with MF = 16 the columns j*16 + 4 (lane / 16) + {0..3}
+    // in acc[i][j][0..3].
+    constexpr int NQ = MF == 32 ? 4 : 1;  // column groups per fragment
+    auto gcol = [&](int j, int q) {        // first column (tile-local) of group q of fragment j
+        return MF == 32 ? j * 32 + 8 * q + 4 * (lane >> 5) : j * 16 + 4 * (lane >> 4);
+    };
 
     // ---- Staged epilogue.  Stored straight from the accumulators, one wavefront
     // instruction would scatter 8- or 16-byte pieces over 32 rows, and with every CU
     // reaching its epilogue at once those partial-line writes run far below HBM rate.
-    // Instead, once the LDS ring is idle, each fragment row i (32 rows of every row block)
+    // Instead, once the LDS ring is idle, each fragment row i (MF rows of every row block)
     // is written to LDS in output layout and the workgroup then stores it in 16-byte
     // chunks, each wavefront instruction covering whole row segments (the residual of
     // ResidAddF32 is read the same way).  The RoPE epilogue stages the fp32 accumulators:
@@ -246,12 +280,12 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     constexpr int SESZ = (F32OUT || ROPE) ? 4 : 2;             // staged element size
     constexpr int ESZ = F32OUT ? 4 : 2;                        // output element size
     constexpr int OCOLS = EPI == Epi::SwiGLU ? BN / 2 : BN;    // output columns per tile
-    constexpr int PROWS = (BM / WM) * 32;                      // rows per pass
+    constexpr int PROWS = (BM / WM) * MF;                      // rows per pass
     constexpr int PITCH = OCOLS * SESZ + 16;                   // staged row, bytes
     constexpr int RCH = OCOLS * SESZ / 16;                     // 16-byte chunks per row
     static_assert(PROWS * PITCH <= NST * S::STAGE * 16, "staging fits the LDS ring");
     char* stg = reinterpret_cast<char*>(lds);
-    const int rl = wm * 32 + (lane & 31);  // staged row of this lane
+    const int rl = wm * MF + lane % MF;  // staged row of this lane
     const int ncol0 = EPI == Epi::SwiGLU ? n0 / 2 : n0;
     const int nlim = EPI == Epi::SwiGLU ? N / 2 : N;
     // RoPE tiles: columns [n0, rot_end) are rotated, [rot_end, n_end) are V columns
@@ -263,24 +297,30 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     for (int i = 0; i < S::FM; ++i) {
         char* srow = stg + rl * PITCH;
         if constexpr (EPI == Epi::SwiGLU) {
+            // gate and up rows of B alternate in 32-row blocks: the gate fragment j pairs
+            // with the up fragment 32 columns on (j + 1 for MF = 32, j + 2 for MF = 16)
+            constexpr int UP = 32 / MF;
 #pragma unroll
-            for (int j = 0; j < S::FN; j += 2)
+            for (int j = 0; j < S::FN; ++j) {
+                if ((j / UP) % 2) continue;  // an up fragment
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
+                for (int q = 0; q < NQ; ++q) {
                     float v[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        v[e] = silu(acc[i][j][4 * q + e]) * acc[i][j + 1][4 * q + e];
-                    const int col = (wn * WN + j * 32) / 2 + 8 * q + 4 * h;
+                        v[e] = silu(acc[i][j][4 * q + e]) * acc[i][j + UP][4 * q + e];
+                    const int gc = wn * WN + gcol(j, q);  // tile column of the gate value
+                    const int col = (gc / 64) * 32 + gc % 32;
                     *reinterpret_cast<uint2*>(srow + col * 2) =
                         make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
                 }
+            }
         } else {
 #pragma unroll
             for (int j = 0; j < S::FN; ++j)
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int col = wn * WN + j * 32 + 8 * q + 4 * h;
+                for (int q = 0; q < NQ; ++q) {
+                    const int col = wn * WN + gcol(j, q);
                     if constexpr (SESZ == 4) {
                         *reinterpret_cast<f32x4*>(srow + col * 4) =
                             f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
@@ -312,7 +352,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
 #pragma unroll
             for (int k = 0; k < NR; ++k) {
                 const int rr = r0 + k * RSTEP;
-                mr[k] = m0 + (rr >> 5) * WM + i * 32 + (rr & 31);
+                mr[k] = m0 + (rr / MF) * WM + i * MF + rr % MF;
                 pr[k] = rot ? rope.pos[min(mr[k], M - 1)] : 0;
             }
             float4 cs[NR][2];
@@ -346,7 +386,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
                 // V dimension, i.e. consecutive columns of one row of V^T
                 static_assert(S::THREADS % PROWS == 0, "token walk");
                 const int rr = tid % PROWS;
-                const int m = m0 + (rr >> 5) * WM + i * 32 + (rr & 31);
+                const int m = m0 + (rr / MF) * WM + i * MF + rr % MF;
                 if (m < M) {
                     const int64_t vc = rope.vcol[m];
                     for (int n2 = rot_end + tid / PROWS; n2 < n_end; n2 += S::THREADS / PROWS) {
@@ -358,7 +398,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
         } else {
             for (int c = tid; c < PROWS * RCH; c += S::THREADS) {
                 const int rr = c / RCH, cc = c - rr * RCH;
-                const int m = m0 + (rr >> 5) * WM + i * 32 + (rr & 31);
+                const int m = m0 + (rr / MF) * WM + i * MF + rr % MF;
                 const int n = ncol0 + cc * (16 / ESZ);
                 if (m >= M || n >= nlim) continue;
                 const uint4 v = *reinterpret_cast<const uint4*>(stg + rr * PITCH + cc * 16);
@@ -560,11 +600,12 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restri
 }
 
 #ifndef SURR_GEMM_KERNELS_ONLY  // (kernel-only builds for standalone tuning harnesses)
-template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI>
+template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI, int MF = 32>
 hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                     int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
     const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    gemm_bf16_kernel<BM, BN, BK, WM, WN, NST, EPI, 8, true><<<(unsigned)tiles, Tile<BM, BN, BK, WM, WN, NST>::THREADS, 0, s>>>(
+    gemm_bf16_kernel<BM, BN, BK, WM, WN, NST, EPI, 8, true, 0, 1, MF>
+        <<<(unsigned)tiles, Tile<BM, BN, BK, WM, WN, NST, MF>::THREADS, 0, s>>>(
         static_cast<const uint16_t*>(A), lda, static_cast<const uint16_t*>(B), ldb, C, ldc, M, N, K,
         rope);
     return hipGetLastError();
@@ -590,8 +631,8 @@ hipError_t run_rows(const void* A, int64_t lda, const void* B, int64_t ldb, void
 }
 
 // Tile choice (measured on the 7B projection shapes): 256 x 256 x 32 tiles, eight
-// wavefronts of 128 x 64 (two per SIMD, so one hides the other's waits), a 3-stage ring
-// and XCD-grouped order; up to 64 rows (decode steps, last-position rows) the few-row
+// wavefronts of 128 x 64 (two per SIMD, so one hides the other's waits) on 16x16x32
+// MFMAs (1-2 points above 32x32x16), a 4-stage ring and XCD-grouped order; up to 64 rows (decode steps, last-position rows) the few-row
 // kernel, up to 128 rows the few-row kernel per 64 rows unless B is wide enough to keep
 // the chip busy with 128 x 128 tiles.
 template <Epi EPI>
@@ -626,7 +667,7 @@ hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
     }
     if (M <= 128)
         return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
-    return run_bf16<256, 256, 32, 128, 64, 3, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+    return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
 }
 
 #endif  // SURR_GEMM_KERNELS_ONLY
