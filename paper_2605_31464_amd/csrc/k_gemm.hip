@@ -462,15 +462,30 @@ __device__ __forceinline__ int rows_slice(int g, int f, const RopeArgs& rope) {
     }
 }
 
-template <int MB, int NF, Epi EPI, int BK>
+template <int MB, int NF, Epi EPI, int BK, bool PAIR = false>
 __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restrict__ A, int64_t lda,
                                                         const uint16_t* __restrict__ B, int64_t ldb,
                                                         void* __restrict__ C, int64_t ldc, int M,
-                                                        int N, int K, RopeArgs rope) {
+                                                        int N, int K, RopeArgs rope, int groups) {
     using R = RowsCfg<MB, NF, EPI, BK>;
     __shared__ uint4 lds[R::NST * R::STAGE];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int g = blockIdx.x;
+    int g = blockIdx.x;
+    if constexpr (PAIR) {
+        // Up to 2 * 16 MB rows: workgroups b and b + 8 take the two row halves of one slice
+        // group.  The hardware deals workgroup b to XCD b % 8, so both run on one XCD at
+        // about the same time and the second reads the weight slices from its L2.
+        const int half = (blockIdx.x >> 3) & 1;
+        g = (blockIdx.x & 7) | ((blockIdx.x >> 4) << 3);
+        const int r0 = 16 * MB * half;
+        if (g >= groups || r0 >= M) return;
+        constexpr int esz = (EPI == Epi::StoreF32 || EPI == Epi::ResidAddF32) ? 4 : 2;
+        A += (int64_t)r0 * lda;
+        C = static_cast<char*>(C) + (int64_t)r0 * ldc * esz;
+        M = min(M - r0, 16 * MB);
+        if (rope.pos) rope.pos += r0;
+        if (rope.vcol) rope.vcol += r0;
+    }
     int slice[NF];
 #pragma unroll
     for (int f = 0; f < NF; ++f) slice[f] = rows_slice<NF, EPI>(g, f, rope);
@@ -611,30 +626,31 @@ hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void
     return hipGetLastError();
 }
 
-template <int MB, Epi EPI>
+template <int MB, Epi EPI, bool PAIR = false>
 hipError_t run_rows(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                     int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
     constexpr int NF = (EPI == Epi::SwiGLU || EPI == Epi::StoreActRope) ? 2 : 1;
-    const unsigned groups = (unsigned)(N / (16 * NF));
+    const int groups = N / (16 * NF);
+    const unsigned grid = PAIR ? (unsigned)(16 * ((groups + 7) / 8)) : (unsigned)groups;
     const uint16_t* a = static_cast<const uint16_t*>(A);
     const uint16_t* b = static_cast<const uint16_t*>(B);
     if constexpr (MB + NF <= 4) {  // 256-column stages while the ring keeps >= 4 of them
         if (K % 256 == 0) {
-            gemm_rows_kernel<MB, NF, EPI, 256><<<groups, RowsCfg<MB, NF, EPI, 256>::THREADS, 0, s>>>(
-                a, lda, b, ldb, C, ldc, M, N, K, rope);
+            gemm_rows_kernel<MB, NF, EPI, 256, PAIR><<<grid, RowsCfg<MB, NF, EPI, 256>::THREADS, 0, s>>>(
+                a, lda, b, ldb, C, ldc, M, N, K, rope, groups);
             return hipGetLastError();
         }
     }
-    gemm_rows_kernel<MB, NF, EPI, 128><<<groups, RowsCfg<MB, NF, EPI, 128>::THREADS, 0, s>>>(
-        a, lda, b, ldb, C, ldc, M, N, K, rope);
+    gemm_rows_kernel<MB, NF, EPI, 128, PAIR><<<grid, RowsCfg<MB, NF, EPI, 128>::THREADS, 0, s>>>(
+        a, lda, b, ldb, C, ldc, M, N, K, rope, groups);
     return hipGetLastError();
 }
 
 // Tile choice (measured on the 7B projection shapes): 256 x 256 x 32 tiles, eight
 // wavefronts of 128 x 64 (two per SIMD, so one hides the other's waits) on 16x16x32
 // MFMAs (1-2 points above 32x32x16), a 4-stage ring and XCD-grouped order; up to 64 rows (decode steps, last-position rows) the few-row
-// kernel, up to 128 rows the few-row kernel per 64 rows unless B is wide enough to keep
-// the chip busy with 128 x 128 tiles.
+// kernel, up to 128 rows the few-row kernel on two 64-row halves unless B is wide enough
+// to keep the chip busy with 128 x 128 tiles.
 template <Epi EPI>
 hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                          int64_t ldc, int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
@@ -648,23 +664,10 @@ hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
         return run_rows<4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
     }
     // 65..128 rows against a narrow B: 128 x 128 tiles would leave most CUs idle (N / 128
-    // workgroups), so the few-row kernel runs once per 64 rows, streaming B twice
-    if (M <= 128 && N < 65536 && rows_ok) {
-        constexpr int esz = (EPI == Epi::StoreF32 || EPI == Epi::ResidAddF32) ? 4 : 2;
-        for (int r0 = 0; r0 < M; r0 += 64) {
-            RopeArgs rp = rope;
-            if (rp.pos) rp.pos += r0;
-            if (rp.vcol) rp.vcol += r0;
-            const int mr = min(64, M - r0);
-            const void* a = static_cast<const uint16_t*>(A) + (int64_t)r0 * lda;
-            void* c = static_cast<char*>(C) + (int64_t)r0 * ldc * esz;
-            const hipError_t e = mr <= 16   ? run_rows<1, EPI>(a, lda, B, ldb, c, ldc, mr, N, K, s, rp)
-                                 : mr <= 32 ? run_rows<2, EPI>(a, lda, B, ldb, c, ldc, mr, N, K, s, rp)
-                                            : run_rows<4, EPI>(a, lda, B, ldb, c, ldc, mr, N, K, s, rp);
-            if (e != hipSuccess) return e;
-        }
-        return hipSuccess;
-    }
+    // workgroups), so the few-row kernel takes the rows in two 64-row halves, paired on
+    // one XCD so each weight slice comes from HBM once
+    if (M <= 128 && N < 65536 && rows_ok)
+        return run_rows<4, EPI, true>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
     if (M <= 128)
         return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
     return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
