@@ -45,6 +45,14 @@ __device__ __forceinline__ int swz(int row) {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.f + __expf(-g)); }
 
+// Fragment rows staged per epilogue pass: the largest power of two (dividing fm) whose
+// rows * pitch bytes fit in the ring.
+constexpr int staged_rows_per_pass(int fm, int rows, int pitch, int ring) {
+    int pg = fm;
+    while (pg > 1 && pg * rows * pitch > ring) pg /= 2;
+    return pg;
+}
+
 // One MFMA step on a 32x32 (16 fp32 per lane) or 16x16 (4 per lane) accumulator.
 __device__ __forceinline__ f32x16 mfma_step(bf16x8 a, bf16x8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -267,10 +275,11 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     // ---- Staged epilogue.  Stored straight from the accumulators, one wavefront
     // instruction would scatter 8- or 16-byte pieces over 32 rows, and with every CU
     // reaching its epilogue at once those partial-line writes run far below HBM rate.
-    // Instead, once the LDS ring is idle, each fragment row i (MF rows of every row block)
-    // is written to LDS in output layout and the workgroup then stores it in 16-byte
-    // chunks, each wavefront instruction covering whole row segments (the residual of
-    // ResidAddF32 is read the same way).  The RoPE epilogue stages the fp32 accumulators:
+    // Instead, once the LDS ring is idle, the accumulators are written to LDS in output
+    // layout, as many fragment rows (MF rows of every row block) per pass as the ring holds,
+    // and the workgroup then stores the pass in 16-byte chunks, each wavefront instruction
+    // covering whole row segments (the residual of ResidAddF32 is read the same way).  Few
+    // passes mean few barriers: the whole SwiGLU tile goes in one pass, fp32 tiles in four.  The RoPE epilogue stages the fp32 accumulators:
     // a chunk and its rotation partner (half a head away, in the same staged row) are
     // combined at store time, so no wavefront needs to hold whole heads; columns of V
     // heads are stored transposed, walking the staged block column by column so that a
@@ -280,10 +289,17 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     constexpr int SESZ = (F32OUT || ROPE) ? 4 : 2;             // staged element size
     constexpr int ESZ = F32OUT ? 4 : 2;                        // output element size
     constexpr int OCOLS = EPI == Epi::SwiGLU ? BN / 2 : BN;    // output columns per tile
-    constexpr int PROWS = (BM / WM) * MF;                      // rows per pass
+    constexpr int FROWS = (BM / WM) * MF;                      // rows of one fragment row i
     constexpr int PITCH = OCOLS * SESZ + 16;                   // staged row, bytes
     constexpr int RCH = OCOLS * SESZ / 16;                     // 16-byte chunks per row
-    static_assert(PROWS * PITCH <= NST * S::STAGE * 16, "staging fits the LDS ring");
+    constexpr int PG = staged_rows_per_pass(S::FM, FROWS, PITCH, NST * S::STAGE * 16);
+    constexpr int PROWS = PG * FROWS;                          // rows per pass
+    static_assert(PROWS * PITCH <= NST * S::STAGE * 16 && S::FM % PG == 0, "staging fits the ring");
+    // staged row rr of the pass starting at fragment row i0 -> output row
+    auto row_of = [&](int rr, int i0) {
+        const int rf = rr % FROWS;
+        return m0 + (rf / MF) * WM + (i0 + rr / FROWS) * MF + rf % MF;
+    };
     char* stg = reinterpret_cast<char*>(lds);
     const int rl = wm * MF + lane % MF;  // staged row of this lane
     const int ncol0 = EPI == Epi::SwiGLU ? n0 / 2 : n0;
@@ -294,8 +310,10 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     const bool vt_cols = ROPE && rope.vt && rot_end < n_end;
     __syncthreads();  // every wavefront is done with the ring
 #pragma unroll
-    for (int i = 0; i < S::FM; ++i) {
-        char* srow = stg + rl * PITCH;
+    for (int i0 = 0; i0 < S::FM; i0 += PG) {
+#pragma unroll
+      for (int i = i0; i < i0 + PG; ++i) {
+        char* srow = stg + ((i - i0) * FROWS + rl) * PITCH;
         if constexpr (EPI == Epi::SwiGLU) {
             // gate and up rows of B alternate in 32-row blocks: the gate fragment j pairs
             // with the up fragment 32 columns on (j + 1 for MF = 32, j + 2 for MF = 16)
@@ -332,6 +350,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
                     }
                 }
         }
+      }
         __syncthreads();
         if constexpr (ROPE) {
             // Rotated q/k columns (and V columns when there is no transposed copy): a
@@ -352,7 +371,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
 #pragma unroll
             for (int k = 0; k < NR; ++k) {
                 const int rr = r0 + k * RSTEP;
-                mr[k] = m0 + (rr / MF) * WM + i * MF + rr % MF;
+                mr[k] = row_of(rr, i0);
                 pr[k] = rot ? rope.pos[min(mr[k], M - 1)] : 0;
             }
             float4 cs[NR][2];
@@ -386,7 +405,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
                 // V dimension, i.e. consecutive columns of one row of V^T
                 static_assert(S::THREADS % PROWS == 0, "token walk");
                 const int rr = tid % PROWS;
-                const int m = m0 + (rr / MF) * WM + i * MF + rr % MF;
+                const int m = row_of(rr, i0);
                 if (m < M) {
                     const int64_t vc = rope.vcol[m];
                     for (int n2 = rot_end + tid / PROWS; n2 < n_end; n2 += S::THREADS / PROWS) {
@@ -398,7 +417,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
         } else {
             for (int c = tid; c < PROWS * RCH; c += S::THREADS) {
                 const int rr = c / RCH, cc = c - rr * RCH;
-                const int m = m0 + (rr / MF) * WM + i * MF + rr % MF;
+                const int m = row_of(rr, i0);
                 const int n = ncol0 + cc * (16 / ESZ);
                 if (m >= M || n >= nlim) continue;
                 const uint4 v = *reinterpret_cast<const uint4*>(stg + rr * PITCH + cc * 16);
