@@ -2,14 +2,16 @@
 //
 // bf16 path: v_mfma_f32_32x32x16_bf16 or v_mfma_f32_16x16x32_bf16 (MF = 32 or 16) on a
 // BM x BN workgroup tile of WM x WN wavefront tiles, K in steps of BK.  Both MFMA shapes
-// accumulate k in the same order and give bitwise the same sums.  Both operands are K-contiguous, so one 16-byte chunk of
-// a row is exactly the 8 consecutive k values an MFMA lane supplies.  Tiles move from
-// HBM straight into LDS with global_load_lds_dwordx4 (no staging registers) through an
-// NST-stage ring, one barrier per K step; LDS rows hold BK/8 chunks whose order is
-// XOR-swizzled by the row to spread the 16-byte reads over the banks.  The MFMA is issued with the weight fragment as its A operand and the
-// activation fragment as its B operand, so each lane ends up owning one output row m
-// and runs of 4 consecutive output columns n.
+// accumulate k in the same order and give bitwise the same sums.  Both operands are
+// K-contiguous, so one 16-byte chunk of a row is exactly the 8 consecutive k values an
+// MFMA lane supplies.  Tiles move from HBM straight into LDS with global_load_lds_dwordx4
+// (no staging registers) through an NST-stage ring, one barrier per K step; LDS rows hold
+// BK/8 chunks whose order is XOR-swizzled by the row to spread the 16-byte reads over the
+// banks.  The MFMA is issued with the weight fragment as its A operand and the activation
+// fragment as its B operand, so each lane ends up owning one output row m and runs of 4
+// consecutive output columns n.
 //
+// Few-row path (decode steps, last-position rows): gemm_rows_kernel below.
 // fp32 path: a plain LDS-tiled FMA kernel for the float32 model.
 #include <type_traits>
 
