@@ -314,6 +314,30 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     const int n_end = min(n0 + BN, N);
     const int rot_end = ROPE ? max(n0, min(n_end, rope.cols)) : n_end;
     const bool vt_cols = ROPE && rope.vt && rot_end < n_end;
+    // Residual add: the fp32 tile takes several passes, and a pass's residual loads would
+    // each wait a full memory round trip after its barrier.  Instead every thread loads
+    // its residual chunks two passes ahead (chunk k of a pass is c = tid + k * THREADS),
+    // so those loads overlap the staging and stores of the passes before.
+    constexpr bool RESID = EPI == Epi::ResidAddF32;
+    constexpr int SWEEP = (PROWS * RCH) / S::THREADS;  // 16-byte chunks per thread and pass
+    constexpr int NPASS = S::FM / PG;
+    f32x4 res[RESID ? 2 : 1][RESID ? SWEEP : 1];
+    auto load_res = [&](int i0, int b) {
+#pragma unroll
+        for (int k = 0; k < SWEEP; ++k) {
+            const int c = tid + k * S::THREADS;
+            const int rr = c / RCH, cc = c - rr * RCH;
+            const int m = row_of(rr, i0);
+            const int n = ncol0 + cc * (16 / ESZ);
+            res[b][k] = (m < M && n < nlim)
+                            ? *reinterpret_cast<const f32x4*>(static_cast<const float*>(C) + (int64_t)m * ldc + n)
+                            : f32x4{};
+        }
+    };
+    if constexpr (RESID) {
+        load_res(0, 0);
+        if constexpr (NPASS > 1) load_res(PG, 1);
+    }
     __syncthreads();  // every wavefront is done with the ring
 #pragma unroll
     for (int i0 = 0; i0 < S::FM; i0 += PG) {
@@ -421,22 +445,26 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
                 }
             }
         } else {
-            // unrolled: every LDS read (and residual load) of the pass is in flight at once
+            // unrolled: every LDS read of the pass is in flight at once
             static_assert((PROWS * RCH) % S::THREADS == 0, "whole store sweeps");
+            const int rb = (i0 / PG) & 1;  // residual buffer of this pass
 #pragma unroll
-            for (int c = tid; c < PROWS * RCH; c += S::THREADS) {
+            for (int k = 0; k < SWEEP; ++k) {
+                const int c = tid + k * S::THREADS;
                 const int rr = c / RCH, cc = c - rr * RCH;
                 const int m = row_of(rr, i0);
                 const int n = ncol0 + cc * (16 / ESZ);
                 if (m >= M || n >= nlim) continue;
                 const uint4 v = *reinterpret_cast<const uint4*>(stg + rr * PITCH + cc * 16);
                 char* g = static_cast<char*>(C) + ((int64_t)m * ldc + n) * ESZ;
-                if constexpr (EPI == Epi::ResidAddF32) {
-                    f32x4* p = reinterpret_cast<f32x4*>(g);
-                    *p = *p + __builtin_bit_cast(f32x4, v);
+                if constexpr (RESID) {
+                    *reinterpret_cast<f32x4*>(g) = res[rb][k] + __builtin_bit_cast(f32x4, v);
                 } else {
                     *reinterpret_cast<uint4*>(g) = v;
                 }
+            }
+            if constexpr (RESID) {
+                if (i0 + 2 * PG < S::FM) load_res(i0 + 2 * PG, rb);
             }
         }
         __syncthreads();
