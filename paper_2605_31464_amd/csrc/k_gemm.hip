@@ -477,7 +477,8 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
 // C = A[M,K] * B[N,K]^T for M <= 16 MB rows (decode steps, last-position rows).  With so
 // few rows the work is reading B once, so each workgroup streams NF 16-row slices of B
 // over the whole K through a deep LDS ring of BK-column stages (direct-to-LDS loads; the
-// ring holds 128 KB, about half of it B), together with the M rows of A; wavefront w < MB
+// ring holds 128 KB, or all 160 KB of LDS for paired single-slice launches, where that
+// measured faster; about half of it B), together with the M rows of A; wavefront w < MB
 // multiplies row block w (v_mfma_f32_16x16x32_bf16).  One barrier per stage: with BK = 256
 // a stage carries 8 dependent MFMA steps, enough to amortise the barrier and the LDS
 // latency (128-column stages halve that and run about half as fast).  Each output still accumulates k in ascending MFMA steps in
@@ -487,14 +488,14 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
 // gate slice and its up slice 32 rows further (gate/up rows interleave in 32-row blocks);
 // RoPE a slice of the first half of a head and its partner half a head further, and, past
 // the rotated columns, two consecutive slices of V columns.
-template <int MB, int NF, Epi EPI, int BK_ = 256>
+template <int MB, int NF, Epi EPI, int BK_ = 256, int RING = 8192>
 struct RowsCfg {
     static constexpr int BK = BK_, CH = BK / 8;          // 16-byte chunks per row and stage
     static constexpr int ROWS_B = 16 * NF, ROWS_A = 16 * MB;
     static constexpr int STAGE = (ROWS_B + ROWS_A) * CH;  // 16-byte slots per stage
     static constexpr int THREADS = 256;
     static constexpr int LOADS = STAGE / THREADS;
-    static constexpr int NST0 = 8192 / STAGE;             // 128 KB of ring
+    static constexpr int NST0 = RING / STAGE;
     static constexpr int NST = NST0 > 16 ? 16 : NST0;
     static_assert(CH >= 16, "swizzle with the row's low 4 bits");
     static_assert(STAGE % THREADS == 0 && (ROWS_B * CH) % 64 == 0, "whole wavefront loads");
@@ -518,12 +519,12 @@ __device__ __forceinline__ int rows_slice(int g, int f, const RopeArgs& rope) {
     }
 }
 
-template <int MB, int NF, Epi EPI, int BK, bool PAIR = false>
+template <int MB, int NF, Epi EPI, int BK, bool PAIR = false, int RING = 8192>
 __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restrict__ A, int64_t lda,
                                                         const uint16_t* __restrict__ B, int64_t ldb,
                                                         void* __restrict__ C, int64_t ldc, int M,
                                                         int N, int K, RopeArgs rope, int groups) {
-    using R = RowsCfg<MB, NF, EPI, BK>;
+    using R = RowsCfg<MB, NF, EPI, BK, RING>;
     __shared__ uint4 lds[R::NST * R::STAGE];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     int g = blockIdx.x;
@@ -690,14 +691,15 @@ hipError_t run_rows(const void* A, int64_t lda, const void* B, int64_t ldb, void
     const unsigned grid = PAIR ? (unsigned)(16 * ((groups + 7) / 8)) : (unsigned)groups;
     const uint16_t* a = static_cast<const uint16_t*>(A);
     const uint16_t* b = static_cast<const uint16_t*>(B);
+    constexpr int RING = PAIR && NF == 1 ? 10240 : 8192;  // 16-byte slots: 160 KB or 128 KB
     if constexpr (MB + NF <= 4) {  // 256-column stages while the ring keeps >= 4 of them
         if (K % 256 == 0) {
-            gemm_rows_kernel<MB, NF, EPI, 256, PAIR><<<grid, RowsCfg<MB, NF, EPI, 256>::THREADS, 0, s>>>(
+            gemm_rows_kernel<MB, NF, EPI, 256, PAIR, RING><<<grid, RowsCfg<MB, NF, EPI, 256, RING>::THREADS, 0, s>>>(
                 a, lda, b, ldb, C, ldc, M, N, K, rope, groups);
             return hipGetLastError();
         }
     }
-    gemm_rows_kernel<MB, NF, EPI, 128, PAIR><<<grid, RowsCfg<MB, NF, EPI, 128>::THREADS, 0, s>>>(
+    gemm_rows_kernel<MB, NF, EPI, 128, PAIR, RING><<<grid, RowsCfg<MB, NF, EPI, 128, RING>::THREADS, 0, s>>>(
         a, lda, b, ldb, C, ldc, M, N, K, rope, groups);
     return hipGetLastError();
 }
@@ -706,7 +708,8 @@ hipError_t run_rows(const void* A, int64_t lda, const void* B, int64_t ldb, void
 // wavefronts of 128 x 64 (two per SIMD, so one hides the other's waits) on 16x16x32
 // MFMAs (1-2 points above 32x32x16), a 4-stage ring and XCD-grouped order; up to 64 rows (decode steps, last-position rows) the few-row
 // kernel, up to 128 rows the few-row kernel on two 64-row halves unless B is wide enough
-// to keep the chip busy with 128 x 128 tiles.
+// to keep the chip busy with 128 x 128 tiles (at 128 rows of the 7B gate/up projection,
+// N = 37,888: 92 us on tiles against 132 us on the few-row kernel).
 template <Epi EPI>
 hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
                          int64_t ldc, int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
@@ -721,8 +724,9 @@ hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
     }
     // 65..128 rows against a narrow B: 128 x 128 tiles would leave most CUs idle (N / 128
     // workgroups), so the few-row kernel takes the rows in two 64-row halves, paired on
-    // one XCD so each weight slice comes from HBM once
-    if (M <= 128 && N < 65536 && rows_ok)
+    // one XCD so each weight slice comes from HBM once.  From N = 32768 (256 tiles, a
+    // workgroup per CU) the tiles are faster.
+    if (M <= 128 && N < 32768 && rows_ok)
         return run_rows<4, EPI, true>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
     if (M <= 128)
         return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);

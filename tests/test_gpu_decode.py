@@ -153,11 +153,17 @@ def test_decode_entries_crossing_key_slices_match_oracle():
     teacher_forced(scorer, W, shape, [250, 509, 1020], 9, seed=77, tol=TOL["bf16"])
 
 
-def test_row_count_regimes_give_bitwise_equal_rows():
+@pytest.mark.parametrize("wide_ffn", [False, True], ids=["d_ff4864", "d_ff16384"])
+def test_row_count_regimes_give_bitwise_equal_rows(wide_ffn):
     """The projections pick a kernel by row count (few-row kernel up to 64 rows, per 64
-    rows up to 128 against narrow weights, tiles above); every choice accumulates in the
-    same order, so a decode step's results do not depend on how many entries share it."""
+    rows up to 128 against narrow weights, 128 x 128 tiles up to 128 rows against weights
+    of 32768 rows or more, 256 x 256 tiles above); every choice accumulates in the same
+    order, so a decode step's results do not depend on how many entries share it.  With
+    d_ff = 16384 the gate/up projection (N = 32768) takes the 128 x 128 tiles with the
+    SwiGLU epilogue from 65 to 128 rows."""
     shape = synth.CONFIGS["small"].shape.replace(n_layers=2)
+    if wide_ffn:
+        shape = shape.replace(n_layers=1, d_ff=16384)
     scorer, W = make_scorer(shape, gain_std=0.1)
     n = 140
     seqs = rng_prompts(shape.vocab, [3 + i % 5 for i in range(n)], 95)
