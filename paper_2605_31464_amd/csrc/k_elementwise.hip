@@ -275,14 +275,12 @@ __global__ __launch_bounds__(256) void capture_rows_kernel(const uint32_t* __res
 // ---------------------------------------------------------------- sequence caches
 // Token j of prompt b (packed row t = cu[b] + j) continues its sequence at position
 // len[b] + j: columns [col0, col0 + words) of row t go to cache row off[b] + len[b] + j.
-__global__ __launch_bounds__(256) void append_rows_kernel(const uint32_t* __restrict__ src,
-                                                          int64_t ld_src, int col0, int words,
-                                                          const int32_t* __restrict__ cu, int B,
-                                                          const int32_t* __restrict__ off,
-                                                          const int32_t* __restrict__ len,
-                                                          uint32_t* __restrict__ dst,
-                                                          int64_t ld_dst) {
-    const int64_t t = blockIdx.x;
+__device__ __forceinline__ void append_row(int64_t t, const uint32_t* __restrict__ src,
+                                           int64_t ld_src, int col0, int words,
+                                           const int32_t* __restrict__ cu, int B,
+                                           const int32_t* __restrict__ off,
+                                           const int32_t* __restrict__ len,
+                                           uint32_t* __restrict__ dst, int64_t ld_dst) {
     int lo = 0, hi = B;
     while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
@@ -294,9 +292,35 @@ __global__ __launch_bounds__(256) void append_rows_kernel(const uint32_t* __rest
     for (int c = threadIdx.x; c < words; c += 256) o[c] = sr[c];
 }
 
+__global__ __launch_bounds__(256) void append_rows_kernel(const uint32_t* __restrict__ src,
+                                                          int64_t ld_src, int col0, int words,
+                                                          const int32_t* __restrict__ cu, int B,
+                                                          const int32_t* __restrict__ off,
+                                                          const int32_t* __restrict__ len,
+                                                          uint32_t* __restrict__ dst,
+                                                          int64_t ld_dst) {
+    append_row(blockIdx.x, src, ld_src, col0, words, cu, B, off, len, dst, ld_dst);
+}
+
 // Transposed V of the same tokens: column vt_off[b] + pi(j) of vt goes to column
 // off[b] + pi(len[b] + j) of the cache's V^T (pi = vt_key_order, applied to the index
 // inside the 64-aligned block of each side).  Block (b, 64-token chunk), threads over rows.
+__device__ __forceinline__ void append_vt_chunk(int b, int j0, const uint16_t* __restrict__ vt,
+                                                int64_t ld_vt, const int32_t* __restrict__ vt_off,
+                                                const int32_t* __restrict__ cu,
+                                                const int32_t* __restrict__ off,
+                                                const int32_t* __restrict__ len, int rows,
+                                                uint16_t* __restrict__ cvt, int64_t ld_c) {
+    const int L = cu[b + 1] - cu[b];
+    if (j0 >= L) return;
+    const int jn = min(64, L - j0), base = len[b];
+    for (int d = threadIdx.x; d < rows; d += 256) {
+        const uint16_t* sr = vt + (int64_t)d * ld_vt + vt_off[b];
+        uint16_t* o = cvt + (int64_t)d * ld_c + off[b];
+        for (int j = j0; j < j0 + jn; ++j) o[vt_key_order(base + j)] = sr[vt_key_order(j)];
+    }
+}
+
 __global__ __launch_bounds__(256) void append_vt_kernel(const uint16_t* __restrict__ vt,
                                                         int64_t ld_vt,
                                                         const int32_t* __restrict__ vt_off,
@@ -305,14 +329,30 @@ __global__ __launch_bounds__(256) void append_vt_kernel(const uint16_t* __restri
                                                         const int32_t* __restrict__ len,
                                                         int rows, uint16_t* __restrict__ cvt,
                                                         int64_t ld_c) {
-    const int b = blockIdx.x, j0 = blockIdx.y * 64;
-    const int L = cu[b + 1] - cu[b];
-    if (j0 >= L) return;
-    const int jn = min(64, L - j0), base = len[b];
-    for (int d = threadIdx.x; d < rows; d += 256) {
-        const uint16_t* sr = vt + (int64_t)d * ld_vt + vt_off[b];
-        uint16_t* o = cvt + (int64_t)d * ld_c + off[b];
-        for (int j = j0; j < j0 + jn; ++j) o[vt_key_order(base + j)] = sr[vt_key_order(j)];
+    append_vt_chunk(blockIdx.x, blockIdx.y * 64, vt, ld_vt, vt_off, cu, off, len, rows, cvt, ld_c);
+}
+
+// Both appends of a bf16 layer in one launch (a decode step's appends are a few rows, so
+// the launch, not the copy, is the cost): blocks [0, T) copy the K row of token t, the
+// rest copy 64-token chunks of V^T, chunks blocks per prompt.
+__global__ __launch_bounds__(256) void append_kv_kernel(const uint32_t* __restrict__ src,
+                                                        int64_t ld_src, int col0, int words,
+                                                        int64_t T, const uint16_t* __restrict__ vt,
+                                                        int64_t ld_vt,
+                                                        const int32_t* __restrict__ vt_off,
+                                                        const int32_t* __restrict__ cu, int B,
+                                                        const int32_t* __restrict__ off,
+                                                        const int32_t* __restrict__ len,
+                                                        uint32_t* __restrict__ ck, int64_t ld_ck,
+                                                        int rows, uint16_t* __restrict__ cvt,
+                                                        int64_t ld_c, int chunks) {
+    const int64_t i = blockIdx.x;
+    if (i < T) {
+        append_row(i, src, ld_src, col0, words, cu, B, off, len, ck, ld_ck);
+    } else {
+        const int64_t v = i - T;
+        append_vt_chunk((int)(v / chunks), (int)(v % chunks) * 64, vt, ld_vt, vt_off, cu, off, len,
+                        rows, cvt, ld_c);
     }
 }
 
@@ -730,6 +770,22 @@ hipError_t launch_append_vt(const uint16_t* vt, int64_t ld_vt, const int32_t* vt
     if (B == 0 || max_len == 0) return hipSuccess;
     append_vt_kernel<<<dim3(B, (max_len + 63) / 64), 256, 0, s>>>(vt, ld_vt, vt_off, cu, off, len,
                                                                  rows, cvt, ld_c);
+    return hipGetLastError();
+}
+
+hipError_t launch_append_kv(const uint16_t* qkv, int64_t ld_qkv, int col0, int cols, int64_t T,
+                            const uint16_t* vt, int64_t ld_vt, const int32_t* vt_off,
+                            const int32_t* cu, int B, int max_len, const int32_t* off,
+                            const int32_t* len, uint16_t* ck, int64_t ld_ck, int rows,
+                            uint16_t* cvt, int64_t ld_c, hipStream_t s) {
+    if (T == 0) return hipSuccess;
+    if (ld_qkv % 2 || col0 % 2 || cols % 2 || ld_ck % 2) return hipErrorInvalidValue;
+    const int chunks = (max_len + 63) / 64;
+    const int64_t blocks = T + (int64_t)B * chunks;
+    if (blocks > INT32_MAX) return hipErrorInvalidValue;
+    append_kv_kernel<<<(unsigned)blocks, 256, 0, s>>>(
+        reinterpret_cast<const uint32_t*>(qkv), ld_qkv / 2, col0 / 2, cols / 2, T, vt, ld_vt, vt_off,
+        cu, B, off, len, reinterpret_cast<uint32_t*>(ck), ld_ck / 2, rows, cvt, ld_c, chunks);
     return hipGetLastError();
 }
 

@@ -67,6 +67,14 @@ hipError_t launch_append_vt(const uint16_t* vt, int64_t ld_vt, const int32_t* vt
                             const int32_t* cu, int B, int max_len, const int32_t* off,
                             const int32_t* len, int rows, uint16_t* cvt, int64_t ld_c,
                             hipStream_t s);
+// Both of a bf16 layer's appends in one launch: the K columns [col0, col0 + cols) of the
+// qkv rows as append_rows (bf16 elements; ld_qkv, col0, cols and ld_ck even) and the
+// `rows` rows of V^T as append_vt.
+hipError_t launch_append_kv(const uint16_t* qkv, int64_t ld_qkv, int col0, int cols, int64_t T,
+                            const uint16_t* vt, int64_t ld_vt, const int32_t* vt_off,
+                            const int32_t* cu, int B, int max_len, const int32_t* off,
+                            const int32_t* len, uint16_t* ck, int64_t ld_ck, int rows,
+                            uint16_t* cvt, int64_t ld_c, hipStream_t s);
 
 // Per row of logits: the first argmax over the vocabulary (next_token, optional) and the
 // full-vocabulary log-softmax at target[b] (target_lp, optional).

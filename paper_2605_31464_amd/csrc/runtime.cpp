@@ -468,11 +468,12 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
             // entries' current lengths, which this layer's attention does not read)
             surrogate_prefix_cache* pc = io.append;
             const int dkv = (int)m->d_kv();
-            SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, surr::launch_append_rows(qkv, dqkv, dq, dkv, (int)m->esz, T, d_cu, batch, d_pfx_off, d_pfx_len, pc->k(l), dkv, stream));
-            if (bf16)
-                SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, surr::launch_append_vt(vt, w.ld_vt, d_vt_off, d_cu, batch, max_len, d_pfx_off, d_pfx_len, dkv, static_cast<uint16_t*>(pc->v(l)), pc->rows, stream));
-            else
+            if (bf16) {
+                SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, surr::launch_append_kv(static_cast<const uint16_t*>(qkv), dqkv, dq, dkv, T, vt, w.ld_vt, d_vt_off, d_cu, batch, max_len, d_pfx_off, d_pfx_len, static_cast<uint16_t*>(pc->k(l)), dkv, dkv, static_cast<uint16_t*>(pc->v(l)), pc->rows, stream));
+            } else {
+                SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, surr::launch_append_rows(qkv, dqkv, dq, dkv, (int)m->esz, T, d_cu, batch, d_pfx_off, d_pfx_len, pc->k(l), dkv, stream));
                 SURR_PHASE_RUN(SURR_PHASE_PREFIX_CAPTURE, surr::launch_append_rows(qkv, dqkv, dq + dkv, dkv, 4, T, d_cu, batch, d_pfx_off, d_pfx_len, pc->v(l), dkv, stream));
+            }
         }
         if (!final_layer) {
             SURR_PHASE_RUN(SURR_PHASE_ATTENTION, surr::launch_attention(a, qkv, dqkv, vt, w.ld_vt, d_vt_off, o, dq, d_cu, d_work, (int)work.size(), nq, nkv, hd, stream, pkp));
