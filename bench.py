@@ -293,7 +293,7 @@ def forecast_head_rates(B, torch, dev, n: int = 65536, reps: int = 200) -> dict:
 
 def cpu_baseline(shape, W, tok, L, vid) -> dict:
     """Time the float64 oracle on a bounded sample of the same workload and scale it to
-    pairs/s: layers 0-7 of the model over the first 1024 tokens of the shortest prompt,
+    pairs/s: layers 0-11 of the model over the first 1024 tokens of the shortest prompt,
     plus one last-position head; scaled linearly in layers and tokens to the batch's
     mean prompt length."""
     from oracle import transformer as ot
@@ -303,7 +303,7 @@ def cpu_baseline(shape, W, tok, L, vid) -> dict:
                        if i.get("user_api") == "blas"] or [os.cpu_count() or 1])
     except Exception:
         threads = os.cpu_count() or 1
-    n_sample_layers, n_tok = 8, 1024
+    n_sample_layers, n_tok = 12, 1024
     i0 = int(np.argmin(L))
     prompt = tok[i0, : min(n_tok, int(L[i0]))]
     arch = dict(n_layers=n_sample_layers, d_model=shape.d_model, n_q_heads=shape.n_q_heads,
