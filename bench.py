@@ -49,8 +49,9 @@ def phase_rates(s, L: np.ndarray, phases: dict, steps: int) -> dict:
     """Achieved rate of each phase against its roofline, from the phase times measured
     with HIP events on the launch stream: MFMA phases in TFLOP/s of algorithmic work,
     memory-bound phases in GB/s of algorithmic bytes (each tensor read or written once).
-    Per step at the batch's lengths: QKV over all T tokens in every layer (the final
-    layer needs every token's K and V); O, gate/up and down over T in the non-final
+    Per step at the batch's lengths: QKV over all T tokens in the non-final layers, and
+    in the final one K/V over all T tokens plus the queries of the B last rows; O, gate/up
+    and down over T in the non-final
     layers; attention on the causal triangle in the non-final layers plus the last row of
     each prompt in the final one; RMSNorm = 2 n_layers - 1 full-batch norms (fp32 row in,
     bf16 row out) plus two on the last rows; the head reads W_head once and writes B rows
@@ -60,7 +61,8 @@ def phase_rates(s, L: np.ndarray, phases: dict, steps: int) -> dict:
     esz = 2 if s.dtype == "bf16" else 4
     Lf = L.astype(np.float64)
     work = {
-        "gemm_qkv": ("mfma", 2.0 * d * (dq + 2 * dkv) * T * nl),
+        "gemm_qkv": ("mfma", 2.0 * d * (dq + 2 * dkv) * T * (nl - 1) + 4.0 * d * dkv * T
+                     + 2.0 * d * dq * B_),
         "gemm_o": ("mfma", 2.0 * dq * d * T * (nl - 1)),
         "gemm_gate_up": ("mfma", 2.0 * d * 2 * ff * T * (nl - 1)),
         "gemm_down": ("mfma", 2.0 * ff * d * T * (nl - 1)),

@@ -248,6 +248,19 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const uint32_t* __rest
     for (int c = threadIdx.x; c < words; c += 256) o[c] = s[c];
 }
 
+// Inverse of gather_rows: row r of src goes to row rows[r] of dst.
+__global__ __launch_bounds__(256) void scatter_rows_kernel(const uint32_t* __restrict__ src,
+                                                           int64_t ld_src,
+                                                           const int32_t* __restrict__ rows,
+                                                           int words,
+                                                           uint32_t* __restrict__ dst,
+                                                           int64_t ld_dst) {
+    const int64_t r = blockIdx.x;
+    const uint32_t* s = src + r * ld_src;
+    uint32_t* o = dst + (int64_t)rows[r] * ld_dst;
+    for (int c = threadIdx.x; c < words; c += 256) o[c] = s[c];
+}
+
 // Row r of a 64-row-aligned cache: prompt b = the last with po[b] <= r, j = r - po[b];
 // copies columns [col0, col0 + words) of packed row cu[b] + j when j < L_b, else zeros.
 __global__ __launch_bounds__(256) void capture_rows_kernel(const uint32_t* __restrict__ src,
@@ -743,6 +756,19 @@ hipError_t launch_gather_rows(const void* src, int64_t ld_src, const int32_t* ro
                                                    ld_src * elem_bytes / 4, rows, words,
                                                    static_cast<uint32_t*>(dst),
                                                    ld_dst * elem_bytes / 4);
+    return hipGetLastError();
+}
+
+hipError_t launch_scatter_rows(const void* src, int64_t ld_src, const int32_t* rows, int64_t n,
+                               int cols, int elem_bytes, void* dst, int64_t ld_dst, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    if ((cols * elem_bytes) % 4 || (ld_src * elem_bytes) % 4 || (ld_dst * elem_bytes) % 4)
+        return hipErrorInvalidValue;
+    scatter_rows_kernel<<<(unsigned)n, 256, 0, s>>>(static_cast<const uint32_t*>(src),
+                                                    ld_src * elem_bytes / 4, rows,
+                                                    cols * elem_bytes / 4,
+                                                    static_cast<uint32_t*>(dst),
+                                                    ld_dst * elem_bytes / 4);
     return hipGetLastError();
 }
 

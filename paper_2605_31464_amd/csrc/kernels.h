@@ -48,6 +48,10 @@ hipError_t launch_swiglu_f32(const float* gu, float* u, int64_t T, int d_ff, hip
 // Copy rows rows[r] of src into dst row r (elem_bytes per element).
 hipError_t launch_gather_rows(const void* src, int64_t ld_src, const int32_t* rows, int64_t n,
                               int cols, int elem_bytes, void* dst, int64_t ld_dst, hipStream_t s);
+// dst[rows[r], :] = src[r, :] for r < n (the inverse of launch_gather_rows; the same
+// 4-byte-multiple width rule).
+hipError_t launch_scatter_rows(const void* src, int64_t ld_src, const int32_t* rows, int64_t n,
+                               int cols, int elem_bytes, void* dst, int64_t ld_dst, hipStream_t s);
 
 // Per prompt b: full-vocab log-softmax of logits[b] at the verdict ids, then the
 // renormalised verdict distribution, its max and first argmax.

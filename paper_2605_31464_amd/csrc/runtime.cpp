@@ -47,7 +47,7 @@ struct LayerW {
 
 // Byte offsets of one call's workspace regions.
 struct WsLayout {
-    size_t cu, last, vid, work, work_last, vt_off, pfx_len, pfx_off, target, dec_items, dec_first,
+    size_t cu, last, pos_last, vid, work, work_last, vt_off, pfx_len, pfx_off, target, dec_items, dec_first,
         dec_prompt, pos, vcol, x, h, qkv, vt, o, u, gu, o_last, x_last, h_last, u_last, gu_last, y,
         logits, dec_part, total;
     int64_t dec_cap;  // decode-attention slice items the workspace holds (bf16 models)
@@ -152,6 +152,7 @@ WsLayout layout(const surrogate_model* m, int64_t B, int64_t T) {
     auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
     w.cu = take(4 * (B + 1));
     w.last = take(4 * B);
+    w.pos_last = take(4 * B);
     w.vid = take(4 * 16);
     w.work = take(8 * items);
     w.work_last = take(8 * B);
@@ -277,9 +278,11 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
     // ---- plan: prompt offsets, last rows, verdict ids, attention work lists
     const int qt = surr::attention_q_tile(m->act);
     std::vector<int32_t> cu(batch + 1, 0), last(batch);
+    std::vector<int32_t> pos_last(batch);
     for (int b = 0; b < batch; ++b) {
         cu[b + 1] = cu[b] + lengths_h[b];
         last[b] = cu[b + 1] - 1;
+        pos_last[b] = plen[b] + lengths_h[b] - 1;  // the position the embedding gives that row
     }
     std::vector<int32_t> vt_off(batch + 1, 0);
     for (int b = 0; b < batch; ++b) vt_off[b + 1] = vt_off[b] + (lengths_h[b] + 63) / 64 * 64;
@@ -328,6 +331,7 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
         char* P = static_cast<char*>(m->pinned);
         std::memcpy(P + w.cu, cu.data(), 4 * cu.size());
         std::memcpy(P + w.last, last.data(), 4 * last.size());
+        std::memcpy(P + w.pos_last, pos_last.data(), 4 * pos_last.size());
         if (n_verdict) std::memcpy(P + w.vid, verdict_ids_h, 4 * (size_t)n_verdict);
         std::memcpy(P + w.work, work.data(), 8 * work.size());
         std::memcpy(P + w.work_last, work_last.data(), 8 * work_last.size());
@@ -348,6 +352,7 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
     char* W = static_cast<char*>(workspace_d);
     const int32_t* d_cu = reinterpret_cast<const int32_t*>(W + w.cu);
     const int32_t* d_last = reinterpret_cast<const int32_t*>(W + w.last);
+    const int32_t* d_pos_last = reinterpret_cast<const int32_t*>(W + w.pos_last);
     const int32_t* d_vid = reinterpret_cast<const int32_t*>(W + w.vid);
     const int2* d_work = reinterpret_cast<const int2*>(W + w.work);
     const int2* d_work_last = reinterpret_cast<const int2*>(W + w.work_last);
@@ -448,7 +453,31 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
             rope.vt = vt;
             rope.ld_vt = w.ld_vt;
             rope.vcol = d_vcol;
-            SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream, rope));
+            // The final layer needs keys and values of every token but queries only at the
+            // last positions (and none when building a prefix cache): the K/V weight rows
+            // run over all tokens, the query rows over the gathered last rows, whose
+            // queries then go to their rows of qkv for the attention below.  Same sums and
+            // roundings as the full projection.  With few tokens per prompt (decode steps)
+            // the full projection is cheaper than the extra launches.
+            const bool q_last_only = final_layer && (io.build || T > 2 * (int64_t)batch);
+            if (!q_last_only) {
+                SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream, rope));
+            } else {
+                surr::RopeArgs rkv = rope;
+                rkv.cols = nkv * hd;  // columns [0, nkv hd) of this product are keys
+                const char* w_kv = static_cast<const char*>(L.w_qkv) + 2 * (size_t)dq * d;
+                SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h, d, w_kv, d, static_cast<char*>(qkv) + 2 * (size_t)dq, dqkv, Ti, dqkv - dq, d, stream, rkv));
+                if (!io.build) {
+                    surr::RopeArgs rq;
+                    rq.pos = d_pos_last;
+                    rq.cs = m->rope_cs;
+                    rq.cols = dq;
+                    rq.head_dim = hd;
+                    SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gather_rows(h, d, d_last, batch, d, 2, h_last, d, stream));
+                    SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h_last, d, L.w_qkv, d, o_last, dq, batch, dq, d, stream, rq));
+                    SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_scatter_rows(o_last, dq, d_last, batch, dq, 2, qkv, dqkv, stream));
+                }
+            }
         } else {
             SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreAct, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream));
             SURR_PHASE_RUN(SURR_PHASE_ROPE, surr::launch_rope(a, qkv, dqkv, T, d_pos, nq + nkv, hd, m->rope_cs, stream));
