@@ -40,9 +40,9 @@ struct Tile {
 // reads at one logical chunk spread over the 16-byte bank groups.  SWZ = 0 puts 16
 // consecutive rows on 16 distinct groups of a 256-byte line; SWZ = 3 ((row / 2) mod CH)
 // puts 8 consecutive 64-byte rows on 8 distinct groups of a 128-byte line, which is what
-// the 16x16x32 fragment reads of 32-column stages (rows l % 16) want: rocprofv3 counts
-// SQ_LDS_BANK_CONFLICT 1.67e9 -> 2.9e7 cycles per 7B gate/up launch and the kernel runs
-// 3% faster.
+// the fragment reads of 32-column stages want (rows l % 16 or l % 32): rocprofv3 counts
+// SQ_LDS_BANK_CONFLICT 1.67e9 -> 2.9e7 cycles per 7B gate/up launch on the 256 x 256
+// tiles, which run 3% faster (the 128 x 128 tiles 1%).
 template <int CH, int SWZ = 0>
 __device__ __forceinline__ int swz(int row) {
     if constexpr (SWZ == 1) return row & (CH - 1);
@@ -746,7 +746,7 @@ hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
     if (M <= 128 && N < 32768 && rows_ok)
         return run_rows<4, EPI, true>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
     if (M <= 128)
-        return run_bf16<128, 128, 32, 64, 64, 4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        return run_bf16<128, 128, 32, 64, 64, 4, EPI, 32, 3>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
     return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16, 3>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
 }
 
