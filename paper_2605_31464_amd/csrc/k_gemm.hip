@@ -100,7 +100,7 @@ __device__ __forceinline__ void tile_coords(int pid, int tiles_m, int tiles_n, i
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI, int GROUP = 8, bool XCD = false,
-          int SWZ = 0, int MINB = 1, int MF = 32>
+          int SWZ = 0, int MINB = 1, int MF = 32, bool ILV = true>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_kernel(const uint16_t* __restrict__ A,
                                                         int64_t lda,
                                                         const uint16_t* __restrict__ B,
@@ -189,7 +189,8 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     // the MFMA rows of the first step of stage kt (its buffer was released by the barrier
     // that opened stage kt), keeping NST-1 stages in flight without stalling MFMA issue.
     // The last step of a stage runs half its MFMA rows, waits for the next stage (vmcnt),
-    // passes the barrier, reads the next stage's first fragments and runs the other half.
+    // passes the barrier and runs the other half, reading the next stage's first fragments
+    // between its MFMAs.
     // With one MFMA step per stage (16x16x32 at BK = 32) the refill goes between the rows
     // of that half, and the fragment buffers alternate between stages (the stage loop is
     // unrolled by two).  sched_barrier pins this order.
@@ -208,6 +209,17 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     bf16x8 fa[2][S::FM], fb[2][S::FN];
     read_a(lds, 0, fa[0]);
     read_b(lds, 0, fb[0]);
+    // Fragment q of MFMA step 0 into buffer nb: B fragments 0..FN-1, then A 0..FM-1.
+    auto read_frag = [&](const uint4* L, int q, int nb) {
+        const int chunk = lane / MF;
+        if (q < S::FN) {
+            const int r = wn * WN + q * MF + lane % MF;
+            fb[nb][q] = __builtin_bit_cast(bf16x8, L[S::A_SLOTS + r * S::CH + (chunk ^ swz<S::CH, SWZ>(r))]);
+        } else {
+            const int r = wm * WM + (q - S::FN) * MF + lane % MF;
+            fa[nb][q - S::FN] = __builtin_bit_cast(bf16x8, L[r * S::CH + (chunk ^ swz<S::CH, SWZ>(r))]);
+        }
+    };
 
     // refill loads [row * LOADS / ROWS, (row + 1) * LOADS / ROWS) after MFMA row `row`
 #define SURR_REFILL_AFTER_ROWS(cb, rows_, rs_, rk_)                                                     \
@@ -250,11 +262,29 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
                 wait_vmcnt<(NST - 2) * S::LOADS>();
                 __syncthreads();
                 const uint4* Ln = lds + ((kt + 1) % NST) * S::STAGE;
-                read_a(Ln, 0, fa[cb ^ 1]);
-                read_b(Ln, 0, fb[cb ^ 1]);
-                __builtin_amdgcn_sched_barrier(0);
-                SURR_MFMA_ROWS(cb, FH, S::FM);
-                __builtin_amdgcn_sched_barrier(0);
+                if constexpr (ILV && KSTEPS == 1) {
+                    // The next stage's fragments (B first, then A in row order) are read
+                    // one or two at a time between this half's MFMAs rather than in one
+                    // burst right after the barrier, when all eight wavefronts would fill
+                    // the LDS command queue at once: 0.8% faster on the gate/up and O
+                    // shapes, bitwise the same results.
+                    constexpr int NR = S::FM + S::FN, NM = (S::FM - FH) * S::FN;
+#pragma unroll
+                    for (int t = 0; t < NM; ++t) {
+                        const int mi = FH + t / S::FN, mj = t % S::FN;
+                        acc[mi][mj] = mfma_step(fb[cb][mj], fa[cb][mi], acc[mi][mj]);
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int q = t * NR / NM; q < (t + 1) * NR / NM; ++q) read_frag(Ln, q, cb ^ 1);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                } else {
+                    read_a(Ln, 0, fa[cb ^ 1]);
+                    read_b(Ln, 0, fb[cb ^ 1]);
+                    __builtin_amdgcn_sched_barrier(0);
+                    SURR_MFMA_ROWS(cb, FH, S::FM);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
         }
     };
