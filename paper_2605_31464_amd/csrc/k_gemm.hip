@@ -708,11 +708,12 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restri
 }
 
 #ifndef SURR_GEMM_KERNELS_ONLY  // (kernel-only builds for standalone tuning harnesses)
-template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI, int MF = 32, int SWZ = 0>
+template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI, int MF = 32, int SWZ = 0,
+          int GROUP = 8>
 hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                     int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
     const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    gemm_bf16_kernel<BM, BN, BK, WM, WN, NST, EPI, 8, true, SWZ, 1, MF>
+    gemm_bf16_kernel<BM, BN, BK, WM, WN, NST, EPI, GROUP, true, SWZ, 1, MF>
         <<<(unsigned)tiles, Tile<BM, BN, BK, WM, WN, NST, MF>::THREADS, 0, s>>>(
         static_cast<const uint16_t*>(A), lda, static_cast<const uint16_t*>(B), ldb, C, ldc, M, N, K,
         rope);
@@ -777,7 +778,17 @@ hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
         return run_rows<4, EPI, true>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
     if (M <= 128)
         return run_bf16<128, 128, 32, 64, 64, 4, EPI, 32, 3>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
-    return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16, 3>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+    // Tile group height (M-tiles per column of the XCD-local block, see tile_coords).  The
+    // tiles that finish together store their outputs together: the fewer M-tiles a group
+    // spans, the longer the row segments of that store.  Narrow outputs gain from short
+    // groups, most of all the fp32 read-modify-write of the residual add (7B O projection
+    // at 262,144 rows: 6.7 ms with groups of 8, 6.0 ms with 2; down 2% faster), while the
+    // wide gate/up projection is fastest with 8.
+    if constexpr (EPI == Epi::ResidAddF32)
+        return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16, 3, 2>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+    if (N <= 8192)
+        return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16, 3, 4>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+    return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16, 3, 8>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
 }
 
 #endif  // SURR_GEMM_KERNELS_ONLY
