@@ -1,0 +1,113 @@
+"""Write the float64 oracle's results for the long-prompt parity cases.
+
+The oracle needs tens of minutes of CPU time per case at these sizes (a 7B-shape
+forward costs about 13 GFLOP per token in float64), too long for a GPU test run, so its
+results are computed once by this script and stored next to it.  The script calls only
+the oracle (``oracle.transformer``) and the seeded input generators (``synth``); no value
+comes from the HIP path.  Each record stores SHA-256 digests of the prompt tokens and of
+the generated weight tensors it read, so a test fails loudly if the generators drift.
+
+Cases:
+* ``oracle_7b_subset.json`` - the 7B-shape benchmark workload (28 layers, d_model 3584,
+  28/4 heads, d_ff 18944, vocab 131072; prompts seed 1, weights seed 0): prompt 0,
+  prompt 1, the shortest and the longest prompt, each at full depth.
+* ``oracle_14b_long.json`` - the 14B-shape width (d_model 5120, 40/8 heads, d_ff 13824,
+  vocab 131072) at 2 layers: prompt 0, the shortest and the longest prompt of the 14B
+  workload (8,417 to 15,979 tokens), and one prompt of max_pos = 16,384 tokens (tokens
+  from seed 3).
+
+Usage: python tests/golden/make_oracle_goldens.py [7b] [14b]   (default: both)
+"""
+from __future__ import annotations
+
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+sys.path.insert(0, ROOT)
+
+from oracle import transformer as ot  # noqa: E402
+from paper_2605_31464_amd import synth  # noqa: E402
+
+LONG_SEED = 3
+N_LAYERS_14B_WIDTH = 2
+
+
+def arch_of(shape):
+    return dict(n_layers=shape.n_layers, d_model=shape.d_model, n_q_heads=shape.n_q_heads,
+                n_kv_heads=shape.n_kv_heads, head_dim=shape.head_dim, d_ff=shape.d_ff,
+                vocab=shape.vocab, rope_base=shape.rope_base, rms_eps=shape.rms_eps)
+
+
+def sha(a) -> str:
+    return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
+
+
+def weights_digest(W, names) -> str:
+    h = hashlib.sha256()
+    for n in names:
+        h.update(np.ascontiguousarray(W[n]).tobytes())
+    return h.hexdigest()
+
+
+def run_rows(shape, W, prompts, vid, labels, out_path, meta):
+    arch = arch_of(shape)
+    names = [s[0] for s in synth.tensor_specs(shape)]
+    rec = dict(meta, verdict_ids=[int(v) for v in vid], weights_sha256=weights_digest(W, names),
+               rows=[])
+    for label, t in zip(labels, prompts):
+        t0 = time.time()
+        r = ot.score(arch, W, [t], vid)
+        dt = time.time() - t0
+        rec["rows"].append(dict(
+            label=label, length=int(len(t)), tokens_sha256=sha(np.asarray(t, np.int32)),
+            logprobs=[float(x) for x in r["logprobs"][0]], p=[float(x) for x in r["p"][0]],
+            confidence=float(r["confidence"][0]), verdict=int(r["verdict"][0]),
+            margin=float(r["margin"][0]), oracle_seconds=round(dt, 1)))
+        print(f"{os.path.basename(out_path)}: {label} (L={len(t)}) done in {dt:.0f} s "
+              f"lp={r['logprobs'][0]}", flush=True)
+        with open(out_path, "w") as f:  # written after every row
+            json.dump(rec, f, indent=1)
+
+
+def case_7b():
+    w = synth.CONFIGS["7b"]
+    tok, L = synth.make_prompts(w)
+    rows = {"prompt 0": 0, "prompt 1": 1, "shortest": int(np.argmin(L)),
+            "longest": int(np.argmax(L))}
+    W = synth.make_weights(w.shape)
+    run_rows(w.shape, W, [tok[i, : L[i]] for i in rows.values()], synth.verdict_ids(w),
+             [f"{k} (row {v})" for k, v in rows.items()],
+             os.path.join(HERE, "oracle_7b_subset.json"),
+             dict(about="float64 oracle on the 7B-shape workload, full depth",
+                  workload=w.name, n_layers=w.shape.n_layers, gain_std=0.0,
+                  prompt_seed=1, weight_seed=0, row_index=list(rows.values())))
+
+
+def case_14b():
+    w = synth.CONFIGS["14b"]
+    shape = w.shape.replace(n_layers=N_LAYERS_14B_WIDTH)
+    tok, L = synth.make_prompts(w)
+    rows = {"prompt 0": 0, "shortest": int(np.argmin(L)), "longest": int(np.argmax(L))}
+    ltok, lL = synth.make_prompts(w, seed=LONG_SEED, lengths=[shape.max_pos])
+    prompts = [tok[i, : L[i]] for i in rows.values()] + [ltok[0, : lL[0]]]
+    labels = [f"{k} (row {v})" for k, v in rows.items()] + [f"max_pos (seed {LONG_SEED})"]
+    W = synth.make_weights(shape)
+    run_rows(shape, W, prompts, synth.verdict_ids(w), labels,
+             os.path.join(HERE, "oracle_14b_long.json"),
+             dict(about=f"float64 oracle at the 14B-shape width, {N_LAYERS_14B_WIDTH} layers, "
+                        "on the 14B workload's long prompts and one max_pos prompt",
+                  workload=w.name, n_layers=N_LAYERS_14B_WIDTH, gain_std=0.0, prompt_seed=1,
+                  long_prompt_seed=LONG_SEED, weight_seed=0, row_index=list(rows.values())))
+
+
+if __name__ == "__main__":
+    which = sys.argv[1:] or ["7b", "14b"]
+    for c in which:
+        {"7b": case_7b, "14b": case_14b}[c]()
