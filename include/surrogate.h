@@ -283,6 +283,24 @@ surrogate_status surrogate_evaluate(const float *probs_d, const float *speedup_d
                                     int32_t *bin_d, float *brier_d, float *crps_d,
                                     double *summary_d, hipStream_t stream);
 
+/* surrogate_evaluate without a workspace argument, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, outputs, limits and errors as surrogate_evaluate; the
+ * caller still provides every input and output buffer.  The workspace is a fixed scratch
+ * array in device memory of 4.5 MiB (room for n = 65536 forecasts with 8 budgets), one per
+ * device, held from the library's loading until the process ends; its device address is
+ * looked up on the first call on each device.  The call allocates nothing: no hipMalloc,
+ * hipFree or allocating library routine.  Calls on one device share that device's
+ * scratch, so calls that overlap on one device (different streams, or threads) race and
+ * must be serialized by the caller.  Nothing carries over between calls: every scratch
+ * byte a call reads it first writes.  Errors: as surrogate_evaluate, and SURR_E_WORKSPACE
+ * if a call would need more than the scratch holds. */
+surrogate_status surrogate_evaluate_noalloc(const float *probs_d, const float *speedup_d, int32_t n,
+                                            int32_t n_bins, const double *bin_values_h,
+                                            const double *bin_edges_h, const double *budgets_h,
+                                            int32_t n_budgets, int32_t *bin_d, float *brier_d,
+                                            float *crps_d, double *summary_d, hipStream_t stream);
+
 /* Synchronize `stream` and report (then clear) the sticky device error of the model:
  * SURR_E_TOKEN_RANGE if an out-of-range token id was seen since the last check. */
 surrogate_status surrogate_device_status(surrogate_model *m, hipStream_t stream);

@@ -30,7 +30,8 @@ EXPORTS = ("surrogate_tensor_count", "surrogate_tensor_shape", "surrogate_load_w
            "surrogate_status_string", "surrogate_last_error", "surrogate_profile_enable",
            "surrogate_profile_collect", "surrogate_forecast_head", "surrogate_prefix_build",
            "surrogate_score_suffixes", "surrogate_prefix_cache_bytes", "surrogate_prefix_free",
-           "surrogate_evaluate_workspace_size", "surrogate_evaluate", "surrogate_cache_create",
+           "surrogate_evaluate_workspace_size", "surrogate_evaluate", "surrogate_evaluate_noalloc",
+           "surrogate_cache_create",
            "surrogate_cache_extend", "surrogate_cache_lengths", "surrogate_cache_reset")
 PHASES = ("embed", "rmsnorm", "gemm_qkv", "rope", "attention", "gemm_o", "gemm_gate_up",
           "gemm_down", "last_rows", "lm_head", "lse_verdict", "prefix_capture")
@@ -89,6 +90,7 @@ def lib() -> ctypes.CDLL:
         "surrogate_cache_lengths": (I32, [P, P]),
         "surrogate_cache_reset": (I32, [P, P, I32]),
         "surrogate_evaluate": (I32, [P, P, I32, I32, P, P, P, I32, P, SZ, P, P, P, P, P]),
+        "surrogate_evaluate_noalloc": (I32, [P, P, I32, I32, P, P, P, I32, P, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -401,6 +403,37 @@ def surrogate_evaluate(probs, speedup, bin_values, bin_edges, budgets=(0.01, 0.0
         e.ctypes.data_as(ctypes.c_void_p), c.ctypes.data_as(ctypes.c_void_p), int(c.size),
         ptr(workspace), workspace.numel() * workspace.element_size(), ptr(bins), ptr(br), ptr(cr),
         ptr(summary), ctypes.c_void_p(_stream(stream))), "surrogate_evaluate")
+    return summary, bins, br, cr
+
+
+def surrogate_evaluate_noalloc(probs, speedup, bin_values, bin_edges,
+                               budgets=(0.01, 0.05, 0.10, 0.25, 0.50), out=None, stream=None):
+    """As surrogate_evaluate, on the library's fixed per-device scratch instead of a workspace.
+    out: optional (summary float64 [8 + n_budgets], bins int32 [n], brier float32 [n], crps
+    float32 [n]) device tensors to write into; the per-candidate ones may be None.  Returns
+    the four tensors."""
+    import torch
+    if probs.dtype != torch.float32 or probs.dim() != 2 or not probs.is_contiguous():
+        raise ValueError("probs must be a contiguous float32 [n, n_bins] device tensor")
+    if speedup.dtype != torch.float32 or speedup.numel() != probs.shape[0]:
+        raise ValueError("speedup must be float32 with one entry per forecast")
+    n, nb = int(probs.shape[0]), int(probs.shape[1])
+    m = np.ascontiguousarray(np.asarray(bin_values, np.float64))
+    e = np.ascontiguousarray(np.asarray(bin_edges, np.float64))
+    c = np.ascontiguousarray(np.asarray(budgets, np.float64))
+    if out is None:
+        dev = probs.device
+        out = (torch.empty(8 + c.size, dtype=torch.float64, device=dev),
+               torch.empty(n, dtype=torch.int32, device=dev),
+               torch.empty(n, dtype=torch.float32, device=dev),
+               torch.empty(n, dtype=torch.float32, device=dev))
+    summary, bins, br, cr = out
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
+    _check(lib().surrogate_evaluate_noalloc(
+        ptr(probs), ptr(speedup), n, nb, m.ctypes.data_as(ctypes.c_void_p),
+        e.ctypes.data_as(ctypes.c_void_p), c.ctypes.data_as(ctypes.c_void_p), int(c.size),
+        ptr(bins), ptr(br), ptr(cr), ptr(summary), ctypes.c_void_p(_stream(stream))),
+        "surrogate_evaluate_noalloc")
     return summary, bins, br, cr
 
 

@@ -539,6 +539,92 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
     return SURR_OK;
 }
 
+// Host-side form of an evaluator call: validated arguments, per-bin constants, the
+// measured count of each budget and the workspace it needs.
+struct EvalCall {
+    surr::EvalBins eb{};
+    surr::BinWeights hw{};
+    int ks[8] = {};
+    size_t need = 0;
+};
+
+surrogate_status evaluate_args(const float* probs_d, const float* speedup_d, int32_t n,
+                               int32_t n_bins, const double* bin_values_h, const double* bin_edges_h,
+                               const double* budgets_h, int32_t n_budgets, double* summary_d,
+                               EvalCall* ec) {
+    if (!probs_d || !speedup_d || !bin_values_h || !bin_edges_h || !budgets_h || !summary_d)
+        return fail(SURR_E_INVALID_ARG, "null argument");
+    if (n_bins < 2 || n_bins > surr::kMaxBins) return fail(SURR_E_INVALID_ARG, "n_bins must be in [2, 16]");
+    const surrogate_status st = surrogate_evaluate_workspace_size(n, n_budgets, &ec->need);
+    if (st != SURR_OK) return st;  // also bounds n_budgets by 8
+    for (int b = 0; b < n_bins; ++b) {
+        if (!std::isfinite(bin_values_h[b])) return fail(SURR_E_INVALID_ARG, "non-finite bin value");
+        ec->eb.value[b] = (float)bin_values_h[b];
+        ec->hw.w[b][0] = (float)bin_values_h[b];
+    }
+    for (int j = 0; j < n_bins - 1; ++j) {
+        if (!std::isfinite(bin_edges_h[j]) || !(bin_edges_h[j] > 0.0) ||
+            (j > 0 && !(bin_edges_h[j] > bin_edges_h[j - 1])))
+            return fail(SURR_E_INVALID_ARG, "bin edges must be finite, positive, strictly increasing");
+        ec->eb.edge[j] = bin_edges_h[j];
+    }
+    for (int c = 0; c < n_budgets; ++c) {
+        if (!(budgets_h[c] > 0.0 && budgets_h[c] <= 1.0)) return fail(SURR_E_INVALID_ARG, "budgets must lie in (0, 1]");
+        ec->ks[c] = std::max(1, (int)std::floor(budgets_h[c] * n));  // top c%, at least one
+    }
+    return SURR_OK;
+}
+
+// The evaluator's launches on a device buffer W of ec.need bytes: expected speedups, per
+// budget the two index lists, the counts, the per-workgroup partial rows.  Every byte it
+// reads was written earlier in the same call, so W needs no clearing.
+surrogate_status evaluate_launch(const EvalCall& ec, const float* probs_d, const float* speedup_d,
+                                 int32_t n, int32_t n_bins, int32_t n_budgets, char* W,
+                                 int32_t* bin_d, float* brier_d, float* crps_d, double* summary_d,
+                                 hipStream_t stream) {
+    float* shat = reinterpret_cast<float*>(W);
+    int32_t* lists = reinterpret_cast<int32_t*>(W + align_up(4 * (size_t)n));
+    int32_t* counts = reinterpret_cast<int32_t*>(W + align_up(4 * (size_t)n) + align_up(8 * (size_t)n * n_budgets));
+    double* partial = reinterpret_cast<double*>(W + align_up(4 * (size_t)n) + align_up(8 * (size_t)n * n_budgets) + align_up(8 * (size_t)n_budgets));
+    SURR_HIP(surr::launch_eval_metrics(probs_d, speedup_d, n, n_bins, ec.eb, bin_d, brier_d, crps_d, partial, stream));
+    SURR_HIP(surr::launch_forecast_head(probs_d, n, n_bins, ec.hw, 0, shat, nullptr, stream));
+    for (int c = 0; c < n_budgets; ++c) {
+        int32_t* d = lists + (size_t)c * 2 * n;
+        SURR_HIP(surr::launch_select(shat, n, 2, 0.f, ec.ks[c], d, d + n, counts + 2 * c, stream));
+    }
+    SURR_HIP(surr::launch_eval_finalize(speedup_d, n, lists, counts, n_budgets, partial, summary_d, stream));
+    return SURR_OK;
+}
+
+// Scratch of surrogate_evaluate_noalloc: room for the evaluator's largest call (65,536
+// forecasts, 8 budgets: 4,536,576 bytes).  Each device the library runs on holds its own
+// copy until the process ends.  Host code never passes the name `scratch` to a kernel or
+// a copy (on the host it is only a stand-in for the device symbol): it takes the device
+// address from device_scratch().
+constexpr size_t kScratchBytes = 4608 * 1024;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_addr[kMaxScratchDevices] = {};
+
+// Device address of the current device's scratch, looked up once per device (with that
+// device current) on the first call that needs it.
+surrogate_status device_scratch(char** out) {
+    int dev = -1;
+    SURR_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxScratchDevices) return fail(SURR_E_HIP, "device ordinal beyond the scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void* p = nullptr;
+        SURR_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) return fail(SURR_E_HIP, "hipGetSymbolAddress returned no address for the scratch");
+        g_scratch_addr[dev] = static_cast<char*>(p);
+    }
+    *out = g_scratch_addr[dev];
+    return SURR_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -964,46 +1050,35 @@ surrogate_status surrogate_evaluate(const float* probs_d, const float* speedup_d
                                     int32_t n_budgets, void* workspace_d, size_t workspace_bytes,
                                     int32_t* bin_d, float* brier_d, float* crps_d,
                                     double* summary_d, hipStream_t stream) {
-    if (!probs_d || !speedup_d || !bin_values_h || !bin_edges_h || !budgets_h || !workspace_d ||
-        !summary_d)
-        return fail(SURR_E_INVALID_ARG, "null argument");
-    if (n_bins < 2 || n_bins > surr::kMaxBins) return fail(SURR_E_INVALID_ARG, "n_bins must be in [2, 16]");
-    size_t need = 0;
-    const surrogate_status st = surrogate_evaluate_workspace_size(n, n_budgets, &need);
+    EvalCall ec;
+    const surrogate_status st = evaluate_args(probs_d, speedup_d, n, n_bins, bin_values_h, bin_edges_h,
+                                              budgets_h, n_budgets, summary_d, &ec);
     if (st != SURR_OK) return st;
-    if (workspace_bytes < need) return fail(SURR_E_WORKSPACE, "workspace needs " + std::to_string(need) + " bytes");
+    if (!workspace_d) return fail(SURR_E_INVALID_ARG, "null argument");
+    if (workspace_bytes < ec.need) return fail(SURR_E_WORKSPACE, "workspace needs " + std::to_string(ec.need) + " bytes");
     if (reinterpret_cast<uintptr_t>(workspace_d) % kAlign) return fail(SURR_E_INVALID_ARG, "workspace must be 256-byte aligned");
-    surr::EvalBins eb{};
-    surr::BinWeights hw{};
-    for (int b = 0; b < n_bins; ++b) {
-        if (!std::isfinite(bin_values_h[b])) return fail(SURR_E_INVALID_ARG, "non-finite bin value");
-        eb.value[b] = (float)bin_values_h[b];
-        hw.w[b][0] = (float)bin_values_h[b];
-    }
-    for (int j = 0; j < n_bins - 1; ++j) {
-        if (!std::isfinite(bin_edges_h[j]) || !(bin_edges_h[j] > 0.0) ||
-            (j > 0 && !(bin_edges_h[j] > bin_edges_h[j - 1])))
-            return fail(SURR_E_INVALID_ARG, "bin edges must be finite, positive, strictly increasing");
-        eb.edge[j] = bin_edges_h[j];
-    }
-    std::vector<int> ks(n_budgets);
-    for (int c = 0; c < n_budgets; ++c) {
-        if (!(budgets_h[c] > 0.0 && budgets_h[c] <= 1.0)) return fail(SURR_E_INVALID_ARG, "budgets must lie in (0, 1]");
-        ks[c] = std::max(1, (int)std::floor(budgets_h[c] * n));  // top c%, at least one
-    }
-    char* W = static_cast<char*>(workspace_d);
-    float* shat = reinterpret_cast<float*>(W);
-    int32_t* lists = reinterpret_cast<int32_t*>(W + align_up(4 * (size_t)n));
-    int32_t* counts = reinterpret_cast<int32_t*>(W + align_up(4 * (size_t)n) + align_up(8 * (size_t)n * n_budgets));
-    double* partial = reinterpret_cast<double*>(W + align_up(4 * (size_t)n) + align_up(8 * (size_t)n * n_budgets) + align_up(8 * (size_t)n_budgets));
-    SURR_HIP(surr::launch_eval_metrics(probs_d, speedup_d, n, n_bins, eb, bin_d, brier_d, crps_d, partial, stream));
-    SURR_HIP(surr::launch_forecast_head(probs_d, n, n_bins, hw, 0, shat, nullptr, stream));
-    for (int c = 0; c < n_budgets; ++c) {
-        int32_t* d = lists + (size_t)c * 2 * n;
-        SURR_HIP(surr::launch_select(shat, n, 2, 0.f, ks[c], d, d + n, counts + 2 * c, stream));
-    }
-    SURR_HIP(surr::launch_eval_finalize(speedup_d, n, lists, counts, n_budgets, partial, summary_d, stream));
-    return SURR_OK;
+    return evaluate_launch(ec, probs_d, speedup_d, n, n_bins, n_budgets, static_cast<char*>(workspace_d),
+                           bin_d, brier_d, crps_d, summary_d, stream);
+}
+
+surrogate_status surrogate_evaluate_noalloc(const float* probs_d, const float* speedup_d, int32_t n,
+                                            int32_t n_bins, const double* bin_values_h,
+                                            const double* bin_edges_h, const double* budgets_h,
+                                            int32_t n_budgets, int32_t* bin_d, float* brier_d,
+                                            float* crps_d, double* summary_d, hipStream_t stream) {
+    EvalCall ec;
+    surrogate_status st = evaluate_args(probs_d, speedup_d, n, n_bins, bin_values_h, bin_edges_h,
+                                        budgets_h, n_budgets, summary_d, &ec);
+    if (st != SURR_OK) return st;
+    if (ec.need > kScratchBytes)
+        return fail(SURR_E_WORKSPACE, "the call needs " + std::to_string(ec.need) +
+                                          " bytes of scratch; the fixed scratch holds " +
+                                          std::to_string(kScratchBytes));
+    char* scratch_d = nullptr;
+    st = device_scratch(&scratch_d);
+    if (st != SURR_OK) return st;
+    return evaluate_launch(ec, probs_d, speedup_d, n, n_bins, n_budgets, scratch_d, bin_d, brier_d,
+                           crps_d, summary_d, stream);
 }
 
 surrogate_status surrogate_device_status(surrogate_model* m, hipStream_t stream) {

@@ -23,7 +23,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = B.lib()
     names = declared_functions()
-    assert len(names) == 24
+    assert len(names) == 25
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B.EXPORTS)
@@ -152,6 +152,19 @@ def test_evaluate_rejects_bad_arguments_synchronously():
     assert call(e_=bad) == B.SURR_E_INVALID_ARG
     assert L.surrogate_evaluate(None, p, 10, 8, m.ctypes.data, e.ctypes.data, c.ctypes.data, 1, p,
                                 1 << 20, None, None, None, p, None) == B.SURR_E_INVALID_ARG
+
+    # the variant on the fixed scratch checks the same arguments before any device call
+    def call_na(n=10, nb=8, m_=m, e_=e, c_=c, probs=p):
+        return L.surrogate_evaluate_noalloc(probs, p, n, nb, m_.ctypes.data, e_.ctypes.data,
+                                            c_.ctypes.data, c_.size, None, None, None, p, None)
+
+    assert call_na(nb=1) == B.SURR_E_INVALID_ARG
+    assert call_na(n=65537) == B.SURR_E_INVALID_ARG  # past the scratch's maximum call
+    assert call_na(n=0) == B.SURR_E_INVALID_ARG
+    assert call_na(c_=np.zeros(9) + 0.5) == B.SURR_E_INVALID_ARG
+    assert call_na(c_=np.array([1.5])) == B.SURR_E_INVALID_ARG
+    assert call_na(e_=bad) == B.SURR_E_INVALID_ARG
+    assert call_na(probs=None) == B.SURR_E_INVALID_ARG
 
 
 def test_cache_calls_reject_bad_arguments_synchronously():
