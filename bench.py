@@ -386,7 +386,7 @@ def main() -> int:
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cfg = B.make_config(s)
-    model = B.surrogate_load_weights(cfg, [W[n] for n in names])
+    model = B.surrogate_load_weights_tensors(cfg, [W[n] for n in names])
     B_ = len(L)
     T = int(L.sum())
     tok = torch.from_numpy(tok_np).to(dev)

@@ -45,8 +45,9 @@ typedef enum {
     SURR_E_TOKEN_RANGE = -3, /* a token id outside [0, vocab) was seen on the device   */
     SURR_E_OOM = -4,         /* device or pinned host allocation failed                  */
     SURR_E_HIP = -5,         /* a HIP runtime call failed                                */
-    SURR_E_WEIGHTS = -6,     /* weight tensor list does not match the config             */
-    SURR_E_WORKSPACE = -7    /* workspace smaller than surrogate_workspace_size()        */
+    SURR_E_WEIGHTS = -6,     /* weight tensor list or weight file does not match the config */
+    SURR_E_WORKSPACE = -7,   /* workspace smaller than surrogate_workspace_size()        */
+    SURR_E_IO = -8           /* weight file cannot be opened or read                     */
 } surrogate_status;
 
 typedef enum { SURR_F32 = 0, SURR_BF16 = 1 } surrogate_dtype;
@@ -75,10 +76,43 @@ typedef struct {
     int32_t dtype;
 } surrogate_config;
 
-/* Number of weight tensors for cfg: 3 + 9 * n_layers. */
+/* Load a model from a weight file (the surrogate of Section 2.1 is a language model prompted
+ * with the forecast query; here a dense decoder with the architecture above).  The file is
+ * little-endian:
+ *   bytes [0, 8)        the magic "SURRWGT1";
+ *   bytes [8, 16)       uint64 H, the length of the JSON header that follows;
+ *   bytes [16, 16 + H)  the header, ASCII JSON:
+ *     {"format": "surrogate-weights", "version": 1,
+ *      "config": {"n_layers", "d_model", "n_q_heads", "n_kv_heads", "head_dim", "d_ff",
+ *                 "vocab", "max_pos", "rope_base", "rms_eps": numbers,
+ *                 "dtype": "bf16" | "f32"},
+ *      "tensors": [{"name": .., "dtype": .., "shape": [rows, cols] ([cols] for norms),
+ *                   "offset": ..}, ...]};
+ *   each tensor's bytes at its offset, a multiple of 4096, tensors in the order below and
+ *   not overlapping (bf16 as raw 16-bit patterns, f32 as IEEE floats, row-major).
+ * Tensor order and names: embed [V, d]; per layer l: layers.l.attn_norm [d],
+ * layers.l.w_qkv [d_q + 2 d_kv, d] (rows: q heads, then k heads, then v heads),
+ * layers.l.w_o [d, d_q], layers.l.mlp_norm [d], layers.l.w_gate [d_ff, d],
+ * layers.l.w_up [d_ff, d], layers.l.w_down [d, d_ff]; final_norm [d]; lm_head [V, d].
+ * Norms are f32; matrices have the config's dtype.  Matrices are [out, in], so both
+ * operands of every projection are contiguous along the reduction.
+ * The whole header is checked before any device work (names, order, dtypes, shapes,
+ * alignment, bounds).  The file is mapped read-only and copied into the model's device
+ * arena; `stream` is synchronized before returning.
+ * Errors: SURR_E_INVALID_ARG (nulls), SURR_E_IO (cannot open or map the file),
+ * SURR_E_WEIGHTS (malformed header or tensors outside the file), SURR_E_SHAPE (config not
+ * supported), SURR_E_OOM, SURR_E_HIP. */
+surrogate_status surrogate_load_weights(const char *path, hipStream_t stream, surrogate_model **out);
+
+/* The configuration a weight file declares, after the same checks surrogate_load_weights
+ * makes on its header and table; no device work (usable without a GPU).
+ * Errors: SURR_E_INVALID_ARG, SURR_E_IO, SURR_E_WEIGHTS. */
+surrogate_status surrogate_weight_file_config(const char *path, surrogate_config *out);
+
+/* Number of weight tensors surrogate_load_weights_tensors takes for cfg: 3 + 9 * n_layers. */
 surrogate_status surrogate_tensor_count(const surrogate_config *cfg, int32_t *n_out);
 
-/* Shape and element type of tensor `index` in the canonical order
+/* Shape and element type of tensor `index` of surrogate_load_weights_tensors, in the order
  *   embed[V, d];
  *   per layer: attn_norm[d], w_q[d_q, d], w_k[d_kv, d], w_v[d_kv, d], w_o[d, d_q],
  *              mlp_norm[d], w_gate[d_ff, d], w_up[d_ff, d], w_down[d, d_ff];
@@ -89,17 +123,19 @@ surrogate_status surrogate_tensor_count(const surrogate_config *cfg, int32_t *n_
 surrogate_status surrogate_tensor_shape(const surrogate_config *cfg, int32_t index,
                                         int64_t *rows, int64_t *cols, int32_t *dtype_out);
 
-/* Create a model from the n_tensors = surrogate_tensor_count() tensors in canonical
- * order.  tensors[i] points to a dense row-major tensor of surrogate_tensor_shape(i);
- * all of them are host memory if tensors_on_device == 0, device memory otherwise.
- * The library copies them into its own device arena (re-laid out for its kernels),
- * builds the RoPE cos/sin table in float64 and stores it as float32, and synchronizes
- * `stream` before returning, so the sources may be freed afterwards.
+/* As surrogate_load_weights from tensors already in memory, for callers that hold the
+ * weights (tests, benchmarks) rather than a file: n_tensors = surrogate_tensor_count()
+ * tensors in the order above; tensors[i] points to a dense row-major tensor of
+ * surrogate_tensor_shape(i); all of them are host memory if tensors_on_device == 0, device
+ * memory otherwise.  The library copies them into its own device arena (re-laid out for its
+ * kernels), builds the RoPE cos/sin table in float64 and stores it as float32, and
+ * synchronizes `stream` before returning, so the sources may be freed afterwards.
  * Errors: SURR_E_INVALID_ARG (nulls), SURR_E_SHAPE (unsupported config),
  * SURR_E_WEIGHTS (n_tensors mismatch), SURR_E_OOM, SURR_E_HIP. */
-surrogate_status surrogate_load_weights(const surrogate_config *cfg, const void *const *tensors,
-                                        int32_t n_tensors, int32_t tensors_on_device,
-                                        hipStream_t stream, surrogate_model **out);
+surrogate_status surrogate_load_weights_tensors(const surrogate_config *cfg,
+                                                const void *const *tensors, int32_t n_tensors,
+                                                int32_t tensors_on_device, hipStream_t stream,
+                                                surrogate_model **out);
 
 surrogate_status surrogate_get_config(const surrogate_model *m, surrogate_config *out);
 

@@ -21,10 +21,12 @@ SURR_E_OOM = -4
 SURR_E_HIP = -5
 SURR_E_WEIGHTS = -6
 SURR_E_WORKSPACE = -7
+SURR_E_IO = -8
 SURR_F32, SURR_BF16 = 0, 1
 SURR_SELECT_THRESHOLD, SURR_SELECT_BUDGET, SURR_SELECT_TOP_SCORE = 0, 1, 2
 
 EXPORTS = ("surrogate_tensor_count", "surrogate_tensor_shape", "surrogate_load_weights",
+           "surrogate_load_weights_tensors", "surrogate_weight_file_config",
            "surrogate_get_config", "surrogate_workspace_size", "surrogate_score_pairs",
            "surrogate_select", "surrogate_device_status", "surrogate_free",
            "surrogate_status_string", "surrogate_last_error", "surrogate_profile_enable",
@@ -68,7 +70,9 @@ def lib() -> ctypes.CDLL:
         "surrogate_tensor_count": (I32, [cfgp, ctypes.POINTER(I32)]),
         "surrogate_tensor_shape": (I32, [cfgp, I32, ctypes.POINTER(I64), ctypes.POINTER(I64),
                                          ctypes.POINTER(I32)]),
-        "surrogate_load_weights": (I32, [cfgp, ctypes.POINTER(P), I32, I32, P, ctypes.POINTER(P)]),
+        "surrogate_load_weights_tensors": (I32, [cfgp, ctypes.POINTER(P), I32, I32, P, ctypes.POINTER(P)]),
+        "surrogate_load_weights": (I32, [ctypes.c_char_p, P, ctypes.POINTER(P)]),
+        "surrogate_weight_file_config": (I32, [ctypes.c_char_p, cfgp]),
         "surrogate_get_config": (I32, [P, cfgp]),
         "surrogate_workspace_size": (I32, [P, I32, I64, I32, ctypes.POINTER(SZ)]),
         "surrogate_score_pairs": (I32, [P, P, I64, P, I32, P, I32, P, SZ, P, P, P, P, P]),
@@ -151,7 +155,25 @@ class Model:
             pass
 
 
-def surrogate_load_weights(cfg: surrogate_config, tensors, stream=None) -> Model:
+def surrogate_load_weights(path, stream=None) -> Model:
+    """A model from a weight file (synth.write_weight_file writes them)."""
+    h = ctypes.c_void_p()
+    _check(lib().surrogate_load_weights(os.fsencode(path), ctypes.c_void_p(_stream(stream)),
+                                        ctypes.byref(h)), "surrogate_load_weights")
+    cfg = surrogate_config()
+    _check(lib().surrogate_get_config(h, ctypes.byref(cfg)), "surrogate_get_config")
+    return Model(h.value, cfg)
+
+
+def surrogate_weight_file_config(path) -> surrogate_config:
+    """The configuration a weight file declares (header checks only, no device work)."""
+    cfg = surrogate_config()
+    _check(lib().surrogate_weight_file_config(os.fsencode(path), ctypes.byref(cfg)),
+           "surrogate_weight_file_config")
+    return cfg
+
+
+def surrogate_load_weights_tensors(cfg: surrogate_config, tensors, stream=None) -> Model:
     """tensors: canonical-order list of numpy host arrays or torch device tensors."""
     n = len(tensors)
     on_device = 0
@@ -175,9 +197,9 @@ def surrogate_load_weights(cfg: surrogate_config, tensors, stream=None) -> Model
     if on_device and any(isinstance(t, np.ndarray) for t in tensors):
         raise ValueError("tensors must be all host arrays or all device tensors")
     h = ctypes.c_void_p()
-    _check(lib().surrogate_load_weights(ctypes.byref(cfg), ptrs, n, on_device,
-                                        ctypes.c_void_p(_stream(stream)), ctypes.byref(h)),
-           "surrogate_load_weights")
+    _check(lib().surrogate_load_weights_tensors(ctypes.byref(cfg), ptrs, n, on_device,
+                                                ctypes.c_void_p(_stream(stream)), ctypes.byref(h)),
+           "surrogate_load_weights_tensors")
     return Model(h.value, cfg)
 
 
@@ -462,13 +484,19 @@ def surrogate_free(model: Model):
 class Scorer:
     """A loaded model plus a workspace sized for one batch shape."""
 
-    def __init__(self, shape, weights: dict, names, device="cuda:0"):
+    def __init__(self, shape, weights: dict, names, device="cuda:0", weight_file=None):
+        """weights/names: tensors in memory; or weight_file: a weight file (shape and
+        weights None)."""
         import torch
         self.torch = torch
         self.device = torch.device(device)
-        self.cfg = make_config(shape)
         with torch.cuda.device(self.device):
-            self.model = surrogate_load_weights(self.cfg, [weights[n] for n in names])
+            if weight_file is not None:
+                self.model = surrogate_load_weights(weight_file)
+                self.cfg = self.model.cfg
+            else:
+                self.cfg = make_config(shape)
+                self.model = surrogate_load_weights_tensors(self.cfg, [weights[n] for n in names])
         self.workspace = None
 
     def ensure_workspace(self, batch, total_tokens, max_len):

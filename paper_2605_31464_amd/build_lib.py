@@ -14,7 +14,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT_DIR = os.path.join(PKG, "lib")
 LIB = os.path.join(OUT_DIR, "libsurrogate.so")
 SOURCES = ["k_elementwise.hip", "k_gemm.hip", "k_attention.hip", "k_forecast.hip", "k_evaluate.hip",
-           "runtime.cpp"]
+           "host.cpp", "runtime.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -11,6 +11,7 @@
 #include <string>
 #include <vector>
 
+#include "host.h"
 #include "kernels.h"
 #include "surrogate.h"
 
@@ -54,44 +55,8 @@ struct WsLayout {
     int64_t ld_vt;  // columns of the transposed V copy (bf16 models)
 };
 
-bool valid_config(const surrogate_config* c, std::string* why) {
-    auto bad = [&](const char* m) { *why = m; return false; };
-    if (c->dtype != SURR_F32 && c->dtype != SURR_BF16) return bad("dtype must be SURR_F32 or SURR_BF16");
-    if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 ||
-        c->d_ff < 1 || c->vocab < 1 || c->max_pos < 1)
-        return bad("sizes must be positive");
-    if (c->n_q_heads % c->n_kv_heads) return bad("n_q_heads must be a multiple of n_kv_heads");
-    if (!(c->rope_base > 0.f) || !(c->rms_eps >= 0.f)) return bad("rope_base > 0 and rms_eps >= 0 required");
-    const int64_t dq = (int64_t)c->n_q_heads * c->head_dim;
-    if (c->dtype == SURR_BF16) {
-        if (c->head_dim != 64 && c->head_dim != 128) return bad("bf16 needs head_dim 64 or 128");
-        if (c->d_model % 64 || dq % 64 || c->d_ff % 64) return bad("bf16 needs d_model, d_q, d_ff multiples of 64");
-    } else {
-        if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
-            return bad("f32 needs head_dim 32, 64 or 128");
-        if (c->d_model % 32 || dq % 32 || c->d_ff % 32) return bad("f32 needs d_model, d_q, d_ff multiples of 32");
-    }
-    if (c->vocab % 32) return bad("vocab must be a multiple of 32");
-    if ((int64_t)c->max_pos * c->vocab <= 0) return bad("overflow");
-    return true;
-}
-
-void tensor_shape(const surrogate_config* c, int idx, int64_t* rows, int64_t* cols, int32_t* dt) {
-    const int64_t d = c->d_model, dq = (int64_t)c->n_q_heads * c->head_dim,
-                  dkv = (int64_t)c->n_kv_heads * c->head_dim, ff = c->d_ff, V = c->vocab;
-    const int last = 1 + 9 * c->n_layers;
-    *dt = c->dtype;
-    if (idx == 0 || idx == last + 1) { *rows = V; *cols = d; return; }
-    if (idx == last) { *rows = 1; *cols = d; *dt = SURR_F32; return; }
-    switch ((idx - 1) % 9) {
-        case 0: case 5: *rows = 1; *cols = d; *dt = SURR_F32; return;
-        case 1: *rows = dq; *cols = d; return;
-        case 2: case 3: *rows = dkv; *cols = d; return;
-        case 4: *rows = d; *cols = dq; return;
-        case 6: case 7: *rows = ff; *cols = d; return;
-        default: *rows = d; *cols = ff; return;
-    }
-}
+using surr::host::tensor_shape;
+using surr::host::valid_config;
 
 }  // namespace
 
@@ -251,20 +216,30 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
         for (int b = 0; b < batch; ++b)
             if (io.target_ids_h[b] < 0 || io.target_ids_h[b] >= c.vocab)
                 return fail(SURR_E_INVALID_ARG, "target id of prompt " + std::to_string(b) + " outside [0, vocab)");
-    // a prompt's positions run to prefix length + length - 1 < max_pos; a prefix leaves
-    // room for at least one continuing token
-    int64_t T = 0;
-    int max_len = 0;
-    for (int b = 0; b < batch; ++b) {
-        max_len = std::max(max_len, lengths_h[b]);
-        const int64_t cap = std::min<int64_t>(std::min<int64_t>(row_stride, room[b]),
-                                              (int64_t)c.max_pos - plen[b] - (io.build ? 1 : 0));
-        if (lengths_h[b] < 1 || lengths_h[b] > cap)
-            return fail(SURR_E_SHAPE, "length of prompt " + std::to_string(b) + (io.build ? " outside [1, min(row_stride, max_pos - 1)]" : io.append ? " outside [1, min(row_stride, max_pos - length, capacity - length)]" : io.prefix ? " outside [1, min(row_stride, max_pos - prefix length)]" : " outside [1, min(row_stride, max_pos)]"));
-        T += lengths_h[b];
+    const bool dec_path = m->act == Act::BF16 && io.append && c.n_q_heads / c.n_kv_heads <= 16 &&
+                          (c.max_pos + surr::attention_decode_slice() - 1) / surr::attention_decode_slice() <=
+                              surr::attention_decode_max_slices();
+    surr::host::PlanArgs pa;
+    pa.lengths = lengths_h;
+    pa.batch = batch;
+    pa.row_stride = row_stride;
+    pa.max_pos = c.max_pos;
+    pa.q_tile = surr::attention_q_tile(m->act);
+    pa.plen = plen.data();
+    pa.room = room.data();
+    pa.build = io.build;
+    pa.append = io.append != nullptr;
+    pa.prefix = io.prefix != nullptr;
+    pa.dec_path = dec_path;
+    pa.dec_slice = surr::attention_decode_slice();
+    surr::host::Plan plan;
+    {
+        std::string why;
+        const surrogate_status ps = surr::host::plan_batch(pa, &plan, &why);
+        if (ps != SURR_OK) return fail(ps, why);
     }
-    if (T + 64 * (int64_t)batch > INT32_MAX)
-        return fail(SURR_E_SHAPE, "total tokens plus 64 per prompt exceed 2^31 - 1");
+    const int64_t T = plan.T;
+    const int max_len = plan.max_len;
     if (reinterpret_cast<uintptr_t>(workspace_d) % kAlign) return fail(SURR_E_INVALID_ARG, "workspace must be 256-byte aligned");
     const WsLayout w = layout(m, batch, T);
     if (workspace_bytes < w.total)
@@ -276,44 +251,16 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
     float* confidence_d = io.confidence_d;
     int32_t* verdict_d = io.verdict_d;
     // ---- plan: prompt offsets, last rows, verdict ids, attention work lists
-    const int qt = surr::attention_q_tile(m->act);
-    std::vector<int32_t> cu(batch + 1, 0), last(batch);
-    std::vector<int32_t> pos_last(batch);
-    for (int b = 0; b < batch; ++b) {
-        cu[b + 1] = cu[b] + lengths_h[b];
-        last[b] = cu[b + 1] - 1;
-        pos_last[b] = plen[b] + lengths_h[b] - 1;  // the position the embedding gives that row
-    }
-    std::vector<int32_t> vt_off(batch + 1, 0);
-    for (int b = 0; b < batch; ++b) vt_off[b + 1] = vt_off[b] + (lengths_h[b] + 63) / 64 * 64;
-    // One-token continuations of cached sequences (decode steps) take the split-key decode
-    // attention; every other prompt takes the tiled kernel.  The choice depends on the
-    // prompt alone, so a row's result does not depend on the batch.
-    const bool dec_path = m->act == Act::BF16 && io.append && c.n_q_heads / c.n_kv_heads <= 16 &&
-                          (c.max_pos + surr::attention_decode_slice() - 1) / surr::attention_decode_slice() <=
-                              surr::attention_decode_max_slices();
-    std::vector<int32_t> dprompt, dfirst(1, 0);
-    std::vector<int2> ditems;
-    std::vector<int2> work, work_last;
-    for (int b = 0; b < batch; ++b) {
-        if (dec_path && lengths_h[b] == 1) {
-            const int ks = surr::attention_decode_slice();
-            const int ns = (plen[b] + 1 + ks - 1) / ks;
-            for (int s2 = 0; s2 < ns; ++s2) ditems.push_back(make_int2((int)dprompt.size(), s2));
-            dprompt.push_back(b);
-            dfirst.push_back((int32_t)ditems.size());
-            continue;
-        }
-        for (int t = 0; t * qt < lengths_h[b]; ++t) work.push_back(make_int2(b, t));
-        work_last.push_back(make_int2(b, (lengths_h[b] - 1) / qt));
-    }
-    // Longest key range first (a cached prefix counts in whole tiles), so the big causal
-    // tiles start early; stable for a deterministic order.
-    auto kv_len = [&](const int2& it) {
-        return (plen[it.x] + 63) / 64 * 64 + std::min(lengths_h[it.x], (it.y + 1) * qt);
-    };
-    std::stable_sort(work.begin(), work.end(),
-                     [&](const int2& a, const int2& b) { return kv_len(a) > kv_len(b); });
+    const std::vector<int32_t>& cu = plan.cu;
+    const std::vector<int32_t>& last = plan.last;
+    const std::vector<int32_t>& pos_last = plan.pos_last;
+    const std::vector<int32_t>& vt_off = plan.vt_off;
+    const std::vector<int32_t>& dprompt = plan.dprompt;
+    const std::vector<int32_t>& dfirst = plan.dfirst;
+    const std::vector<surr::host::Int2>& ditems = plan.ditems;
+    const std::vector<surr::host::Int2>& work = plan.work;
+    const std::vector<surr::host::Int2>& work_last = plan.work_last;
+    static_assert(sizeof(surr::host::Int2) == sizeof(int2), "work items are copied as int2");
 
     const size_t meta_bytes = w.pos;  // cu .. vt_off are contiguous from offset 0
     {
@@ -658,9 +605,9 @@ void surrogate_free(surrogate_model* m) {
     delete m;
 }
 
-surrogate_status surrogate_load_weights(const surrogate_config* cfg, const void* const* tensors,
-                                        int32_t n_tensors, int32_t tensors_on_device,
-                                        hipStream_t stream, surrogate_model** out) {
+surrogate_status surrogate_load_weights_tensors(const surrogate_config* cfg, const void* const* tensors,
+                                                int32_t n_tensors, int32_t tensors_on_device,
+                                                hipStream_t stream, surrogate_model** out) {
     if (!cfg || !tensors || !out) return fail(SURR_E_INVALID_ARG, "null argument");
     *out = nullptr;
     std::string why;
@@ -757,6 +704,55 @@ surrogate_status surrogate_load_weights(const surrogate_config* cfg, const void*
     }
     *out = m;
     return SURR_OK;
+}
+
+surrogate_status surrogate_weight_file_config(const char* path, surrogate_config* out) {
+    if (!path || !out) return fail(SURR_E_INVALID_ARG, "null argument");
+    surr::host::MappedFile f;
+    std::string why;
+    if (!surr::host::map_file(path, &f, &why)) return fail(SURR_E_IO, why);
+    surr::host::WeightFile wf;
+    const bool ok = surr::host::parse_weight_file(f.data, f.size, f.size, &wf, &why);
+    surr::host::unmap_file(&f);
+    if (!ok) return fail(SURR_E_WEIGHTS, std::string(path) + ": " + why);
+    *out = wf.cfg;
+    return SURR_OK;
+}
+
+surrogate_status surrogate_load_weights(const char* path, hipStream_t stream, surrogate_model** out) {
+    if (!path || !out) return fail(SURR_E_INVALID_ARG, "null argument");
+    *out = nullptr;
+    surr::host::MappedFile f;
+    std::string why;
+    if (!surr::host::map_file(path, &f, &why)) return fail(SURR_E_IO, why);
+    surr::host::WeightFile wf;
+    if (!surr::host::parse_weight_file(f.data, f.size, f.size, &wf, &why)) {
+        surr::host::unmap_file(&f);
+        return fail(SURR_E_WEIGHTS, std::string(path) + ": " + why);
+    }
+    // The file's fused w_qkv rows are the q, k and v matrices back to back: the tensor list
+    // of surrogate_load_weights_tensors points into it.
+    const surrogate_config& c = wf.cfg;
+    const size_t e = c.dtype == SURR_BF16 ? 2 : 4, d = c.d_model;
+    const size_t dq = (size_t)c.n_q_heads * c.head_dim, dkv = (size_t)c.n_kv_heads * c.head_dim;
+    std::vector<const void*> t;
+    t.reserve(3 + 9 * (size_t)c.n_layers);
+    auto at = [&](int i) { return static_cast<const void*>(f.data + wf.tensors[i].offset); };
+    t.push_back(at(0));
+    for (int l = 0; l < c.n_layers; ++l) {
+        const int b = 1 + 7 * l;
+        const unsigned char* qkv = f.data + wf.tensors[b + 1].offset;
+        t.push_back(at(b));                      // attn_norm
+        t.push_back(qkv);                        // w_q
+        t.push_back(qkv + dq * d * e);           // w_k
+        t.push_back(qkv + (dq + dkv) * d * e);   // w_v
+        for (int k = 2; k < 7; ++k) t.push_back(at(b + k));  // w_o, mlp_norm, w_gate, w_up, w_down
+    }
+    t.push_back(at(1 + 7 * c.n_layers));      // final_norm
+    t.push_back(at(2 + 7 * c.n_layers));      // lm_head
+    const surrogate_status st = surrogate_load_weights_tensors(&c, t.data(), (int32_t)t.size(), 0, stream, out);
+    surr::host::unmap_file(&f);  // the load has synchronized the stream
+    return st;
 }
 
 surrogate_status surrogate_get_config(const surrogate_model* m, surrogate_config* out) {
@@ -1125,7 +1121,8 @@ const char* surrogate_status_string(surrogate_status s) {
         case SURR_E_TOKEN_RANGE: return "token id out of range";
         case SURR_E_OOM: return "out of memory";
         case SURR_E_HIP: return "HIP runtime error";
-        case SURR_E_WEIGHTS: return "weights do not match the config";
+        case SURR_E_WEIGHTS: return "weights do not match the config, or a malformed weight file";
+        case SURR_E_IO: return "weight file unreadable";
         case SURR_E_WORKSPACE: return "workspace too small";
     }
     return "unknown status";

@@ -171,6 +171,66 @@ def make_weights(shape: ModelShape, seed: int = 0, gain_std: float = 0.0,
     return out
 
 
+FILE_MAGIC = b"SURRWGT1"
+FILE_ALIGN = 4096
+
+
+def file_tensors(shape: ModelShape, weights: dict) -> list:
+    """(name, dtype, shape, array) of every tensor in weight-file order: the per-layer
+    q, k and v matrices are stored as one w_qkv matrix (q rows, then k, then v)."""
+    dt = shape.dtype
+    out = [("embed", dt, list(weights["embed"].shape), weights["embed"])]
+    for l in range(shape.n_layers):
+        p = f"layers.{l}."
+        qkv = np.concatenate([weights[p + "w_q"], weights[p + "w_k"], weights[p + "w_v"]], axis=0)
+        out += [(p + "attn_norm", "f32", [shape.d_model], weights[p + "attn_norm"]),
+                (p + "w_qkv", dt, list(qkv.shape), qkv),
+                (p + "w_o", dt, list(weights[p + "w_o"].shape), weights[p + "w_o"]),
+                (p + "mlp_norm", "f32", [shape.d_model], weights[p + "mlp_norm"])]
+        out += [(p + n, dt, list(weights[p + n].shape), weights[p + n])
+                for n in ("w_gate", "w_up", "w_down")]
+    out += [("final_norm", "f32", [shape.d_model], weights["final_norm"]),
+            ("lm_head", dt, list(weights["lm_head"].shape), weights["lm_head"])]
+    return out
+
+
+def write_weight_file(path, shape: ModelShape, weights: dict) -> None:
+    """Write a weight file: the magic, the header length (uint64 little-endian), the JSON
+    header (config and tensor table), then each tensor's raw little-endian bytes at an
+    offset that is a multiple of 4096 (bf16 as 16-bit patterns, f32 as IEEE floats)."""
+    import json
+    entries = file_tensors(shape, weights)
+    config = {"n_layers": shape.n_layers, "d_model": shape.d_model,
+              "n_q_heads": shape.n_q_heads, "n_kv_heads": shape.n_kv_heads,
+              "head_dim": shape.head_dim, "d_ff": shape.d_ff, "vocab": shape.vocab,
+              "max_pos": shape.max_pos, "rope_base": float(shape.rope_base),
+              "rms_eps": float(shape.rms_eps), "dtype": shape.dtype}
+
+    def header(start):
+        table, off = [], start
+        for name, dt, shp, a in entries:
+            table.append({"name": name, "dtype": dt, "shape": shp, "offset": off})
+            off += -(-np.asarray(a).nbytes // FILE_ALIGN) * FILE_ALIGN
+        return json.dumps({"format": "surrogate-weights", "version": 1, "config": config,
+                           "tensors": table}).encode("ascii")
+
+    start = FILE_ALIGN
+    while True:  # the first tensor starts at the first 4096 boundary past the header
+        h = header(start)
+        need = -(-(16 + len(h)) // FILE_ALIGN) * FILE_ALIGN
+        if need == start:
+            break
+        start = need
+    with open(path, "wb") as f:
+        f.write(FILE_MAGIC + len(h).to_bytes(8, "little") + h)
+        for (name, dt, shp, a), t in zip(entries, json.loads(h)["tensors"]):
+            a = np.ascontiguousarray(a, np.float32 if dt == "f32" else np.uint16)
+            if a.size != int(np.prod(shp)):
+                raise ValueError(f"{name}: {a.size} elements, shape {shp}")
+            f.seek(t["offset"])
+            f.write(a.astype(a.dtype.newbyteorder("<"), copy=False).tobytes())
+
+
 def zipf_cdf(vocab: int, s: float = 1.1) -> np.ndarray:
     r = np.arange(1, vocab + 1, dtype=np.float64)
     c = np.cumsum(r ** -s)

@@ -23,7 +23,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = B.lib()
     names = declared_functions()
-    assert len(names) == 25
+    assert len(names) == 27
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B.EXPORTS)
@@ -55,7 +55,7 @@ def test_load_weights_rejects_wrong_tensor_count_before_allocating():
     cfg = B.make_config(synth.CONFIGS["tiny"].shape)
     ptrs = (ctypes.c_void_p * 3)(1, 1, 1)
     h = ctypes.c_void_p()
-    st = B.lib().surrogate_load_weights(ctypes.byref(cfg), ptrs, 3, 0, None, ctypes.byref(h))
+    st = B.lib().surrogate_load_weights_tensors(ctypes.byref(cfg), ptrs, 3, 0, None, ctypes.byref(h))
     assert st == B.SURR_E_WEIGHTS and not h.value
     assert b"expected" in B.lib().surrogate_last_error()
 
@@ -192,7 +192,7 @@ def test_score_pairs_rejects_null_model():
 
 def test_status_strings():
     L = B.lib()
-    for s in range(0, -8, -1):
+    for s in range(0, -9, -1):
         assert L.surrogate_status_string(s)
     assert L.surrogate_status_string(-3) == b"token id out of range"
 
@@ -204,3 +204,102 @@ def test_library_has_no_unresolved_kernel_stubs():
     out = subprocess.run(["nm", "-D", "--undefined-only", B.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     assert "__device_stub__" not in out
+
+
+# ---------------------------------------------------------------- weight files
+def _config_tuple(cfg):
+    return tuple(getattr(cfg, f) for f, _ in B.surrogate_config._fields_)
+
+
+@pytest.mark.parametrize("name,layers", [("tiny", 2), ("small", 1), ("7b", 1)])
+def test_weight_file_round_trip_config(tmp_path, name, layers):
+    """synth.write_weight_file writes the format the library reads: the declared
+    configuration comes back field for field, the tensor bytes sit where the header says."""
+    shape = synth.CONFIGS[name].shape.replace(n_layers=layers)
+    if name == "7b":  # full width, a tiny vocabulary keeps the file small
+        shape = shape.replace(vocab=256)
+    W = synth.make_weights(shape, gain_std=0.1)
+    path = tmp_path / "w.surw"
+    synth.write_weight_file(path, shape, W)
+    got = B.surrogate_weight_file_config(str(path))
+    assert _config_tuple(got) == _config_tuple(B.make_config(shape))
+    raw = path.read_bytes()
+    assert raw[:8] == b"SURRWGT1"
+    hl = int.from_bytes(raw[8:16], "little")
+    import json
+    head = json.loads(raw[16:16 + hl])
+    for (n, dt, shp, a), t in zip(synth.file_tensors(shape, W), head["tensors"]):
+        assert t["name"] == n and t["offset"] % 4096 == 0
+        a = np.ascontiguousarray(a)
+        assert raw[t["offset"]: t["offset"] + a.nbytes] == a.tobytes(), n
+
+
+def _mutations(raw):
+    """Malformed variants of a valid file, each with what is wrong."""
+    import json
+    hl = int.from_bytes(raw[8:16], "little")
+    head = json.loads(raw[16:16 + hl])
+    first = head["tensors"][0]["offset"]
+
+    def with_header(h):  # the blobs stay where the original offsets put them
+        hb = json.dumps(h).encode()
+        out = raw[:8] + len(hb).to_bytes(8, "little") + hb
+        return out + bytes(first - len(out)) + raw[first:] if len(out) <= first else None
+
+    def edit(fn):
+        h = json.loads(json.dumps(head))
+        fn(h)
+        return with_header(h)
+
+    yield "bad magic", b"XURRWGT1" + raw[8:]
+    yield "truncated preamble", raw[:10]
+    yield "header length past the end", raw[:8] + (len(raw)).to_bytes(8, "little") + raw[16:]
+    yield "header length zero", raw[:8] + (0).to_bytes(8, "little") + raw[16:]
+    yield "truncated last tensor", raw[:-100]
+    yield "broken JSON", raw[:16 + hl // 2] + b"}" + raw[16 + hl // 2 + 1:]
+    yield "wrong format", edit(lambda h: h.update(format="other"))
+    yield "wrong version", edit(lambda h: h.update(version=2))
+    yield "missing config field", edit(lambda h: h["config"].pop("d_ff"))
+    yield "extra config field", edit(lambda h: h["config"].update(extra=1))
+    yield "bad dtype", edit(lambda h: h["config"].update(dtype="f16"))
+    yield "unsupported shape", edit(lambda h: h["config"].update(head_dim=48))
+    yield "fractional size", edit(lambda h: h["config"].update(d_model=128.5))
+    yield "tensor missing", edit(lambda h: h["tensors"].pop())
+    yield "tensors swapped", edit(lambda h: h["tensors"].__setitem__(
+        slice(1, 3), [h["tensors"][2], h["tensors"][1]]))
+    yield "wrong tensor dtype", edit(lambda h: h["tensors"][1].update(dtype="bf16"))
+    yield "wrong shape", edit(lambda h: h["tensors"][2].update(
+        shape=[h["tensors"][2]["shape"][0] + 1, h["tensors"][2]["shape"][1]]))
+    yield "misaligned offset", edit(lambda h: h["tensors"][3].update(offset=h["tensors"][3]["offset"] + 8))
+    yield "overlapping tensors", edit(lambda h: h["tensors"][3].update(offset=h["tensors"][2]["offset"]))
+    yield "negative offset", edit(lambda h: h["tensors"][0].update(offset=-4096))
+    yield "offset past the end", edit(lambda h: h["tensors"][-1].update(offset=1 << 40))
+    yield "extra tensor key", edit(lambda h: h["tensors"][0].update(extra=0))
+
+
+def test_malformed_weight_files_are_rejected_before_device_work(tmp_path):
+    shape = synth.CONFIGS["tiny"].shape
+    W = synth.make_weights(shape)
+    good = tmp_path / "good.surw"
+    synth.write_weight_file(good, shape, W)
+    raw = good.read_bytes()
+    L = B.lib()
+    cfg = B.surrogate_config()
+    h = ctypes.c_void_p()
+    seen = 0
+    for what, data in _mutations(raw):
+        if data is None:
+            continue
+        p = tmp_path / "bad.surw"
+        p.write_bytes(data)
+        assert L.surrogate_weight_file_config(str(p).encode(), ctypes.byref(cfg)) == B.SURR_E_WEIGHTS, what
+        # the loader checks the same header before it touches a device
+        assert L.surrogate_load_weights(str(p).encode(), None, ctypes.byref(h)) == B.SURR_E_WEIGHTS, what
+        assert not h.value
+        seen += 1
+    assert seen >= 20
+    assert L.surrogate_weight_file_config(str(tmp_path / "none.surw").encode(),
+                                          ctypes.byref(cfg)) == B.SURR_E_IO
+    assert L.surrogate_weight_file_config(str(tmp_path).encode(), ctypes.byref(cfg)) == B.SURR_E_IO
+    assert L.surrogate_weight_file_config(None, ctypes.byref(cfg)) == B.SURR_E_INVALID_ARG
+    assert L.surrogate_load_weights(None, None, ctypes.byref(h)) == B.SURR_E_INVALID_ARG

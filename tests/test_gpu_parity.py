@@ -257,3 +257,25 @@ def test_small_config_full_depth_sampled_prompts():
     d, a, c = B.surrogate_select(out["confidence"], B.SURR_SELECT_BUDGET, budget_k=k)
     assert_selection_valid(out["confidence"].cpu().numpy(), d.cpu().numpy(), a.cpu().numpy(),
                            c.cpu().numpy(), "budget", k=k)
+
+
+# ---------------------------------------------------------------- weight files
+@pytest.mark.parametrize("name,layers", [("tiny", 2), ("small", 2)])
+def test_weight_file_model_scores_like_the_tensor_model(tmp_path, name, layers):
+    """A model loaded from a weight file (q/k/v fused in the file, split on loading) is the
+    model loaded from the same tensors in memory: bitwise equal outputs."""
+    shape = synth.CONFIGS[name].shape.replace(n_layers=layers)
+    W = synth.make_weights(shape, gain_std=0.1)
+    path = tmp_path / f"{name}.surw"
+    synth.write_weight_file(path, shape, W)
+    mem = B.Scorer(shape, W, [s[0] for s in synth.tensor_specs(shape)], DEV)
+    fil = B.Scorer(None, None, None, DEV, weight_file=str(path))
+    for f, _ in B.surrogate_config._fields_:
+        assert getattr(fil.cfg, f) == getattr(mem.cfg, f), f
+    tok, L = padded(rng_prompts(shape.vocab, [1, 64, 129, 300], 23))
+    vid = [0, 1, shape.vocab - 1]
+    a, b = mem.score(tok, L, vid), fil.score(tok, L, vid)
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+    if name == "tiny":
+        assert_parity(b, oracle_for(shape, W, tok, L, vid), TOL["f32"])
