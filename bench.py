@@ -54,12 +54,14 @@ def phase_rates(s, L: np.ndarray, phases: dict, steps: int) -> dict:
     and down over T in the non-final
     layers; attention on the causal triangle in the non-final layers plus the last row of
     each prompt in the final one; RMSNorm = 2 n_layers - 1 full-batch norms (fp32 row in,
-    bf16 row out) plus two on the last rows; the head reads W_head once and writes B rows
-    of logits; embedding gathers bf16 rows into the fp32 residual."""
+    bf16 row out) plus two on the last rows; the head reads W_head once (bf16 models write
+    one 16-byte record per row and 128-column tile, the float32 model B rows of logits) and
+    the read-out reads those back; embedding gathers bf16 rows into the fp32 residual."""
     d, dq, dkv, ff, V = s.d_model, s.d_q, s.d_kv, s.d_ff, s.vocab
     nl, T, B_ = s.n_layers, float(L.sum()), float(len(L))
     esz = 2 if s.dtype == "bf16" else 4
     Lf = L.astype(np.float64)
+    head_out = B_ * (16 * ((V + 127) // 128) if s.dtype == "bf16" else 4 * V)
     work = {
         "gemm_qkv": ("mfma", 2.0 * d * (dq + 2 * dkv) * T * (nl - 1) + 4.0 * d * dkv * T
                      + 2.0 * d * dq * B_),
@@ -70,8 +72,8 @@ def phase_rates(s, L: np.ndarray, phases: dict, steps: int) -> dict:
                       + float((4 * s.n_q_heads * s.head_dim * Lf).sum())),
         "embed": ("hbm", T * (esz * d + 4 * d + 12)),
         "rmsnorm": ("hbm", ((2 * nl - 1) * T + 2 * B_) * (4 * d + esz * d)),
-        "lm_head": ("hbm", esz * V * d + esz * B_ * d + 4 * B_ * V),
-        "lse_verdict": ("hbm", 4 * B_ * V),
+        "lm_head": ("hbm", esz * V * d + esz * B_ * d + head_out),
+        "lse_verdict": ("hbm", head_out),
     }
     out = {}
     for ph, (bound, amount) in work.items():

@@ -149,7 +149,13 @@ surrogate_status surrogate_workspace_size(const surrogate_model *m, int32_t batc
  *                lengths_h[i] entries; entries beyond are never read.
  *  lengths_h     host int32 [batch]; 1 <= lengths_h[i] <= min(row_stride, max_pos).
  *  verdict_ids_h host int32 [n_verdict], 1 <= n_verdict <= 16, distinct ids in [0, vocab).
- *  workspace_d   device buffer of >= surrogate_workspace_size() bytes, 256-byte aligned.
+ *  workspace_d   device buffer, 256-byte aligned, of workspace_bytes bytes.  With at least
+ *                surrogate_workspace_size(m, batch, sum of lengths, max length) bytes the
+ *                batch runs as one pass.  A smaller workspace (a token budget) makes the
+ *                call score consecutive chunks of whole prompts, each the longest run of
+ *                prompts that fits; outputs are the same, since a prompt's outputs do not
+ *                depend on the other prompts.  The least workable size is that of the
+ *                longest prompt alone, surrogate_workspace_size(m, 1, L, L).
  * Outputs (device, caller-owned):
  *  logprobs_d    float [batch, n_verdict]: log-softmax over the full vocabulary of the
  *                next-token logits at position lengths_h[i] - 1, at the verdict ids.
@@ -160,7 +166,7 @@ surrogate_status surrogate_workspace_size(const surrogate_model *m, int32_t batc
  * surrogate_device_status() reports as SURR_E_TOKEN_RANGE.  Results are deterministic:
  * a prompt's outputs do not depend on the other prompts of the batch or on the run.
  * Errors (synchronous, nothing enqueued): SURR_E_INVALID_ARG, SURR_E_SHAPE,
- * SURR_E_WORKSPACE, SURR_E_OOM (pinned staging), SURR_E_HIP. */
+ * SURR_E_WORKSPACE (a prompt alone does not fit), SURR_E_OOM (pinned staging), SURR_E_HIP. */
 surrogate_status surrogate_score_pairs(surrogate_model *m, const int32_t *tokens_d,
                                        int64_t row_stride, const int32_t *lengths_h,
                                        int32_t batch, const int32_t *verdict_ids_h,
@@ -192,7 +198,8 @@ surrogate_status surrogate_prefix_build(surrogate_model *m, const int32_t *token
  * Every output equals that of surrogate_score_pairs on the concatenated prompt, up to
  * rounding order.  Positions continue after the prefix, so prefix length + lengths_h[i]
  * <= max_pos.  Workspace: surrogate_workspace_size(m, batch, sum of lengths_h, max of
- * lengths_h).  The cache must come from the same model.
+ * lengths_h), or less, down to the longest prompt alone (chunked as in
+ * surrogate_score_pairs).  The cache must come from the same model.
  * Errors as surrogate_score_pairs; SURR_E_INVALID_ARG for a prefix id outside
  * [-1, n_prefix) or a cache of another model. */
 surrogate_status surrogate_score_suffixes(surrogate_model *m, const surrogate_prefix_cache *cache,

@@ -1,5 +1,7 @@
 // Bandwidth-bound kernels: embedding gather, RMSNorm, RoPE, fp32 SwiGLU, row gather,
 // full-vocab log-softmax + verdict read-out, and selective deferral.
+#include <climits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -460,6 +462,36 @@ __global__ __launch_bounds__(kLseThreads) void lse_next_kernel(const float* __re
     }
 }
 
+// Verdict read-out of row b from its verdict logits zv[0 .. nv) and the full-vocabulary
+// log-sum-exp: lp_v = zv[v] - lse, p = softmax(lp), q = max p and the first argmax.
+__device__ void verdict_readout(const float* zv, int nv, float lse, int b, float* lp,
+                                float* probs, float* conf, int32_t* verdict) {
+    float l[16];
+    float m2 = -INFINITY;
+    for (int v = 0; v < nv; ++v) {
+        l[v] = zv[v] - lse;
+        lp[b * nv + v] = l[v];
+        m2 = fmaxf(m2, l[v]);
+    }
+    float se = 0.f;
+    for (int v = 0; v < nv; ++v) {
+        l[v] = expf(l[v] - m2);
+        se += l[v];
+    }
+    int best = 0;
+    float q = -1.f;
+    for (int v = 0; v < nv; ++v) {
+        const float p = l[v] / se;
+        if (probs) probs[b * nv + v] = p;
+        if (p > q) {
+            q = p;
+            best = v;
+        }
+    }
+    conf[b] = q;
+    if (verdict) verdict[b] = best;
+}
+
 // ---------------------------------------------------------------- LSE + verdicts
 // One workgroup per prompt.  LSE = max + log(sum exp(z - max)) over the full vocabulary
 // (fixed-order reductions), lp_v = z[vid_v] - LSE, then p = softmax(lp), q = max p and
@@ -479,31 +511,68 @@ __global__ __launch_bounds__(kLseThreads) void lse_verdict_kernel(const float* _
     int am;
     row_lse<false>(z, V, red, redi, lse, am);
     if (threadIdx.x == 0) {
-        float l[16];
-        float m2 = -INFINITY;
-        for (int v = 0; v < nv; ++v) {
-            l[v] = z[vid[v]] - lse;
-            lp[b * nv + v] = l[v];
-            m2 = fmaxf(m2, l[v]);
-        }
-        float se = 0.f;
-        for (int v = 0; v < nv; ++v) {
-            l[v] = expf(l[v] - m2);
-            se += l[v];
-        }
-        int best = 0;
-        float q = -1.f;
-        for (int v = 0; v < nv; ++v) {
-            const float p = l[v] / se;
-            if (probs) probs[b * nv + v] = p;
-            if (p > q) {
-                q = p;
-                best = v;
-            }
-        }
-        conf[b] = q;
-        if (verdict) verdict[b] = best;
+        float zv[16];
+        for (int v = 0; v < nv; ++v) zv[v] = z[vid[v]];
+        verdict_readout(zv, nv, lse, b, lp, probs, conf, verdict);
     }
+}
+
+// ---------------------------------------------------------------- LSE from tile records
+// One workgroup per row merges the row's n_tiles records (max m_t, sum s_t of exp(z - m_t),
+// first argmax a_t) written by the LM head's Epi::LseTile epilogue: thread t folds tiles
+// t, t + 256, ... in order, then the partials merge by a fixed butterfly inside each wave
+// and in wave order, so the result does not depend on timing.  The merge of (m1, s1, a1)
+// and (m2, s2, a2) is (max, s1 e^(m1 - max) + s2 e^(m2 - max), the argmax of the larger
+// maximum, the lower index on a tie).
+constexpr int kCombThreads = 256, kCombWaves = kCombThreads / 64;
+
+struct LseRec {
+    float m, s;
+    int a;
+};
+
+__device__ __forceinline__ LseRec lse_merge(LseRec x, LseRec y) {
+    const float nm = fmaxf(x.m, y.m);
+    const float sx = x.m > -INFINITY ? x.s * expf(x.m - nm) : 0.f;
+    const float sy = y.m > -INFINITY ? y.s * expf(y.m - nm) : 0.f;
+    LseRec r;
+    r.a = y.m > x.m ? y.a : (x.m > y.m ? x.a : min(x.a, y.a));
+    r.s = sx + sy;
+    r.m = nm;
+    return r;
+}
+
+__global__ __launch_bounds__(kCombThreads) void lse_combine_kernel(
+    const float4* __restrict__ part, int n_tiles, const float* __restrict__ picked, int nv,
+    float* __restrict__ lp, float* __restrict__ probs, float* __restrict__ conf,
+    int32_t* __restrict__ verdict, int32_t* __restrict__ next_token, float* __restrict__ target_lp) {
+    __shared__ LseRec red[kCombWaves];
+    const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const float4* rp = part + (int64_t)b * n_tiles;
+    LseRec acc{-INFINITY, 0.f, INT_MAX};
+    for (int t = tid; t < n_tiles; t += kCombThreads) {
+        const float4 r = rp[t];
+        acc = lse_merge(acc, LseRec{r.x, r.y, __float_as_int(r.z)});
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        LseRec other{__shfl_xor(acc.m, o, 64), __shfl_xor(acc.s, o, 64), __shfl_xor(acc.a, o, 64)};
+        acc = lse_merge(acc, other);
+    }
+    if (lane == 0) red[wave] = acc;
+    __syncthreads();
+    if (tid != 0) return;
+    LseRec tot = red[0];
+    for (int w = 1; w < kCombWaves; ++w) tot = lse_merge(tot, red[w]);
+    const float lse = tot.m + logf(tot.s);
+    const float* pk = picked + (int64_t)b * kPicked;
+    if (nv > 0) {
+        float zv[kMaxVerdicts];
+        for (int v = 0; v < nv; ++v) zv[v] = pk[v];
+        verdict_readout(zv, nv, lse, b, lp, probs, conf, verdict);
+    }
+    if (next_token) next_token[b] = tot.a;
+    if (target_lp) target_lp[b] = pk[kMaxVerdicts] - lse;
 }
 
 // ---------------------------------------------------------------- selection
@@ -812,6 +881,15 @@ hipError_t launch_append_kv(const uint16_t* qkv, int64_t ld_qkv, int col0, int c
     append_kv_kernel<<<(unsigned)blocks, 256, 0, s>>>(
         reinterpret_cast<const uint32_t*>(qkv), ld_qkv / 2, col0 / 2, cols / 2, T, vt, ld_vt, vt_off,
         cu, B, off, len, reinterpret_cast<uint32_t*>(ck), ld_ck / 2, rows, cvt, ld_c, chunks);
+    return hipGetLastError();
+}
+
+hipError_t launch_lse_combine(const float4* part, int n_tiles, const float* picked, int B, int nv,
+                              float* lp, float* probs, float* conf, int32_t* verdict,
+                              int32_t* next_token, float* target_lp, hipStream_t s) {
+    if (B <= 0) return hipSuccess;
+    lse_combine_kernel<<<B, kCombThreads, 0, s>>>(part, n_tiles, picked, nv, lp, probs, conf, verdict,
+                                                  next_token, target_lp);
     return hipGetLastError();
 }
 

@@ -13,6 +13,7 @@
 //
 // Few-row path (decode steps, last-position rows): gemm_rows_kernel below.
 // fp32 path: a plain LDS-tiled FMA kernel for the float32 model.
+#include <climits>
 #include <type_traits>
 
 #include "common.h"
@@ -106,7 +107,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
                                                         const uint16_t* __restrict__ B,
                                                         int64_t ldb, void* __restrict__ C,
                                                         int64_t ldc, int M, int N, int K,
-                                                        RopeArgs rope) {
+                                                        EpiArgs ep) {
     using S = Tile<BM, BN, BK, WM, WN, NST, MF>;
     using Acc = typename std::conditional<MF == 32, f32x16, f32x4>::type;
     __shared__ uint4 lds[NST * S::STAGE];
@@ -327,8 +328,9 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     // heads are stored transposed, walking the staged block column by column so that a
     // wavefront instruction writes 64 consecutive tokens of one row of V^T.
     constexpr bool ROPE = EPI == Epi::StoreActRope;
+    constexpr bool LSE = EPI == Epi::LseTile;
     constexpr bool F32OUT = EPI == Epi::StoreF32 || EPI == Epi::ResidAddF32;
-    constexpr int SESZ = (F32OUT || ROPE) ? 4 : 2;             // staged element size
+    constexpr int SESZ = (F32OUT || ROPE || LSE) ? 4 : 2;      // staged element size
     constexpr int ESZ = F32OUT ? 4 : 2;                        // output element size
     constexpr int OCOLS = EPI == Epi::SwiGLU ? BN / 2 : BN;    // output columns per tile
     constexpr int FROWS = (BM / WM) * MF;                      // rows of one fragment row i
@@ -348,8 +350,8 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
     const int nlim = EPI == Epi::SwiGLU ? N / 2 : N;
     // RoPE tiles: columns [n0, rot_end) are rotated, [rot_end, n_end) are V columns
     const int n_end = min(n0 + BN, N);
-    const int rot_end = ROPE ? max(n0, min(n_end, rope.cols)) : n_end;
-    const bool vt_cols = ROPE && rope.vt && rot_end < n_end;
+    const int rot_end = ROPE ? max(n0, min(n_end, ep.cols)) : n_end;
+    const bool vt_cols = ROPE && ep.vt && rot_end < n_end;
     // Residual add: the fp32 tile takes several passes, and a pass's residual loads would
     // each wait a full memory round trip after its barrier.  Instead every thread loads
     // its residual chunks two passes ahead (chunk k of a pass is c = tid + k * THREADS),
@@ -424,12 +426,12 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
             // cos/sin values of all its rows are loaded before any is used.
             static_assert(S::THREADS % RCH == 0 && PROWS % (S::THREADS / RCH) == 0, "chunk walk");
             constexpr int RSTEP = S::THREADS / RCH, NR = PROWS / RSTEP;
-            const int hd = rope.head_dim, half = hd >> 1;
+            const int hd = ep.head_dim, half = hd >> 1;
             const int lim = vt_cols ? rot_end : n_end;
             const int cc = tid % RCH, r0 = tid / RCH;
             const int n = n0 + cc * 4;
             const int hi = n % hd;  // the 4 columns lie inside one half of a head
-            const bool lo = hi < half, rot = n < rope.cols;
+            const bool lo = hi < half, rot = n < ep.cols;
             const int poff = (lo ? half : -half) * 4;  // partner chunk, bytes
             const int coff = lo ? hi : hi - half;
             int mr[NR];
@@ -438,12 +440,12 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
             for (int k = 0; k < NR; ++k) {
                 const int rr = r0 + k * RSTEP;
                 mr[k] = row_of(rr, i0);
-                pr[k] = rot ? rope.pos[min(mr[k], M - 1)] : 0;
+                pr[k] = rot ? ep.pos[min(mr[k], M - 1)] : 0;
             }
             float4 cs[NR][2];
 #pragma unroll
             for (int k = 0; k < NR; ++k) {
-                const float4* t = reinterpret_cast<const float4*>(rope.cs + (int64_t)pr[k] * half + coff);
+                const float4* t = reinterpret_cast<const float4*>(ep.cs + (int64_t)pr[k] * half + coff);
                 cs[k][0] = rot ? t[0] : float4{1.f, 0.f, 1.f, 0.f};
                 cs[k][1] = rot ? t[1] : float4{1.f, 0.f, 1.f, 0.f};
             }
@@ -473,12 +475,65 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
                 const int rr = tid % PROWS;
                 const int m = row_of(rr, i0);
                 if (m < M) {
-                    const int64_t vc = rope.vcol[m];
+                    const int64_t vc = ep.vcol[m];
                     for (int n2 = rot_end + tid / PROWS; n2 < n_end; n2 += S::THREADS / PROWS) {
                         const float v = *reinterpret_cast<const float*>(stg + rr * PITCH + (n2 - n0) * 4);
-                        rope.vt[(int64_t)(n2 - rope.cols) * rope.ld_vt + vc] = (uint16_t)f32_to_bf16(v);
+                        ep.vt[(int64_t)(n2 - ep.cols) * ep.ld_vt + vc] = (uint16_t)f32_to_bf16(v);
                     }
                 }
+            }
+        } else if constexpr (LSE) {
+            // LM-head read-out: per staged row the tile's max, first argmax and sum of
+            // exp(z - max) over its valid columns.  TPR consecutive threads share a row,
+            // each walking CPT columns in order; their partials merge by a butterfly (the
+            // same sums on both lanes of a pair: addition commutes), so the record does not
+            // depend on timing.
+            constexpr int TPR = S::THREADS / PROWS, CPT = OCOLS / TPR;
+            static_assert(S::THREADS % PROWS == 0 && TPR <= 64 && (TPR & (TPR - 1)) == 0 &&
+                              OCOLS % TPR == 0, "row split");
+            const HeadArgs& hd = ep.head;
+            const int rr = tid / TPR, q = tid % TPR;
+            const int m = row_of(rr, i0);
+            const float* srow = reinterpret_cast<const float*>(stg + rr * PITCH);
+            const int c0 = q * CPT;
+            float mx = -INFINITY;
+            int am = INT_MAX;
+            for (int c = c0; c < c0 + CPT; ++c)
+                if (n0 + c < N && srow[c] > mx) {
+                    mx = srow[c];
+                    am = n0 + c;
+                }
+            float sum = 0.f;
+            if (mx > -INFINITY)
+                for (int c = c0; c < c0 + CPT; ++c)
+                    if (n0 + c < N) sum += expf(srow[c] - mx);
+#pragma unroll
+            for (int o = 1; o < TPR; o <<= 1) {
+                const float om = __shfl_xor(mx, o, 64), os = __shfl_xor(sum, o, 64);
+                const int oa = __shfl_xor(am, o, 64);
+                const float nm = fmaxf(mx, om);
+                const float a1 = mx > -INFINITY ? sum * expf(mx - nm) : 0.f;
+                const float a2 = om > -INFINITY ? os * expf(om - nm) : 0.f;
+                am = om > mx ? oa : (mx > om ? am : min(am, oa));
+                sum = a1 + a2;
+                mx = nm;
+            }
+            if (q == 0 && m < M)
+                hd.part[(int64_t)m * tiles_n + tn] = make_float4(mx, sum, __int_as_float(am), 0.f);
+            // the logits at the shared verdict ids and at each row's own target id
+            for (int idx = tid; idx < PROWS * kPicked; idx += S::THREADS) {
+                const int r2 = idx / kPicked, v = idx - r2 * kPicked;
+                const int m2 = row_of(r2, i0);
+                if (m2 >= M) continue;
+                int col = -1;
+                if (v < kMaxVerdicts) {
+                    if (v < hd.n_vid) col = hd.vid[v];
+                } else if (hd.target) {
+                    col = hd.target[m2];
+                }
+                if (col >= n0 && col < n_end)
+                    hd.picked[(int64_t)m2 * kPicked + v] =
+                        *reinterpret_cast<const float*>(stg + r2 * PITCH + (col - n0) * 4);
             }
         } else {
             // unrolled: every LDS read of the pass is in flight at once
@@ -540,16 +595,16 @@ struct RowsCfg {
 };
 
 template <int NF, Epi EPI>
-__device__ __forceinline__ int rows_slice(int g, int f, const RopeArgs& rope) {
+__device__ __forceinline__ int rows_slice(int g, int f, const EpiArgs& ep) {
     if constexpr (EPI == Epi::SwiGLU) {
         return 64 * (g >> 1) + 16 * (g & 1) + 32 * f;
     } else if constexpr (EPI == Epi::StoreActRope) {
-        const int rot_groups = rope.cols / 32;
+        const int rot_groups = ep.cols / 32;
         if (g < rot_groups) {
-            const int half = rope.head_dim >> 1, per_head = half / 16;
-            return (g / per_head) * rope.head_dim + 16 * (g % per_head) + half * f;
+            const int half = ep.head_dim >> 1, per_head = half / 16;
+            return (g / per_head) * ep.head_dim + 16 * (g % per_head) + half * f;
         }
-        return rope.cols + 32 * (g - rot_groups) + 16 * f;
+        return ep.cols + 32 * (g - rot_groups) + 16 * f;
     } else {
         return 16 * (g * NF + f);
     }
@@ -559,7 +614,7 @@ template <int MB, int NF, Epi EPI, int BK, bool PAIR = false, int RING = 8192>
 __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restrict__ A, int64_t lda,
                                                         const uint16_t* __restrict__ B, int64_t ldb,
                                                         void* __restrict__ C, int64_t ldc, int M,
-                                                        int N, int K, RopeArgs rope, int groups) {
+                                                        int N, int K, EpiArgs ep, int groups) {
     using R = RowsCfg<MB, NF, EPI, BK, RING>;
     __shared__ uint4 lds[R::NST * R::STAGE];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -576,12 +631,12 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restri
         A += (int64_t)r0 * lda;
         C = static_cast<char*>(C) + (int64_t)r0 * ldc * esz;
         M = min(M - r0, 16 * MB);
-        if (rope.pos) rope.pos += r0;
-        if (rope.vcol) rope.vcol += r0;
+        if (ep.pos) ep.pos += r0;
+        if (ep.vcol) ep.vcol += r0;
     }
     int slice[NF];
 #pragma unroll
-    for (int f = 0; f < NF; ++f) slice[f] = rows_slice<NF, EPI>(g, f, rope);
+    for (int f = 0; f < NF; ++f) slice[f] = rows_slice<NF, EPI>(g, f, ep);
     const char* b_base = reinterpret_cast<const char*>(B + (int64_t)slice[0] * ldb);
     const char* a_base = reinterpret_cast<const char*>(A);
     // Load j of this thread fills slot (wave * LOADS + j) * 64 + lane of a stage: slots
@@ -656,10 +711,10 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restri
         *reinterpret_cast<uint2*>(static_cast<uint16_t*>(C) + (int64_t)m * ldc + col) =
             make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
     } else if constexpr (EPI == Epi::StoreActRope) {
-        if (slice[0] < rope.cols) {
-            const int hd = rope.head_dim, half = hd >> 1;
+        if (slice[0] < ep.cols) {
+            const int hd = ep.head_dim, half = hd >> 1;
             const int i0 = slice[0] % hd + 4 * ck;  // first-half index of this lane's 4 columns
-            const float4* t = reinterpret_cast<const float4*>(rope.cs + (int64_t)rope.pos[m] * half + i0);
+            const float4* t = reinterpret_cast<const float4*>(ep.cs + (int64_t)ep.pos[m] * half + i0);
             const float4 t0 = t[0], t1 = t[1];
             const float c4[4] = {t0.x, t0.z, t1.x, t1.z};
             const float s4[4] = {t0.y, t0.w, t1.y, t1.w};
@@ -678,11 +733,11 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restri
 #pragma unroll
             for (int f = 0; f < NF; ++f) {
                 const int n = slice[f] + 4 * ck;
-                if (rope.vt) {
-                    const int64_t vc = rope.vcol[m];
+                if (ep.vt) {
+                    const int64_t vc = ep.vcol[m];
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        rope.vt[(int64_t)(n + e - rope.cols) * rope.ld_vt + vc] = (uint16_t)f32_to_bf16(acc[f][e]);
+                        ep.vt[(int64_t)(n + e - ep.cols) * ep.ld_vt + vc] = (uint16_t)f32_to_bf16(acc[f][e]);
                 } else {
                     *reinterpret_cast<uint2*>(static_cast<uint16_t*>(C) + (int64_t)m * ldc + n) =
                         make_uint2(pack_bf16x2(acc[f][0], acc[f][1]), pack_bf16x2(acc[f][2], acc[f][3]));
@@ -711,18 +766,18 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restri
 template <int BM, int BN, int BK, int WM, int WN, int NST, Epi EPI, int MF = 32, int SWZ = 0,
           int GROUP = 8>
 hipError_t run_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
-                    int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
+                    int M, int N, int K, hipStream_t s, const EpiArgs& ep) {
     const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
     gemm_bf16_kernel<BM, BN, BK, WM, WN, NST, EPI, GROUP, true, SWZ, 1, MF>
         <<<(unsigned)tiles, Tile<BM, BN, BK, WM, WN, NST, MF>::THREADS, 0, s>>>(
         static_cast<const uint16_t*>(A), lda, static_cast<const uint16_t*>(B), ldb, C, ldc, M, N, K,
-        rope);
+        ep);
     return hipGetLastError();
 }
 
 template <int MB, Epi EPI, bool PAIR = false>
 hipError_t run_rows(const void* A, int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
-                    int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
+                    int M, int N, int K, hipStream_t s, const EpiArgs& ep) {
     constexpr int NF = (EPI == Epi::SwiGLU || EPI == Epi::StoreActRope) ? 2 : 1;
     const int groups = N / (16 * NF);
     const unsigned grid = PAIR ? (unsigned)(16 * ((groups + 7) / 8)) : (unsigned)groups;
@@ -736,19 +791,19 @@ hipError_t run_rows(const void* A, int64_t lda, const void* B, int64_t ldb, void
         // Narrow weights (< 256 groups) lose with it and keep the deep ring.
         if (groups >= 512) {
             gemm_rows_kernel<MB, NF, EPI, 128, false, 4096><<<grid, RowsCfg<MB, NF, EPI, 128, 4096>::THREADS, 0, s>>>(
-                a, lda, b, ldb, C, ldc, M, N, K, rope, groups);
+                a, lda, b, ldb, C, ldc, M, N, K, ep, groups);
             return hipGetLastError();
         }
     }
     if constexpr (MB + NF <= 4) {  // 256-column stages while the ring keeps >= 4 of them
         if (K % 256 == 0) {
             gemm_rows_kernel<MB, NF, EPI, 256, PAIR, RING><<<grid, RowsCfg<MB, NF, EPI, 256, RING>::THREADS, 0, s>>>(
-                a, lda, b, ldb, C, ldc, M, N, K, rope, groups);
+                a, lda, b, ldb, C, ldc, M, N, K, ep, groups);
             return hipGetLastError();
         }
     }
     gemm_rows_kernel<MB, NF, EPI, 128, PAIR, RING><<<grid, RowsCfg<MB, NF, EPI, 128, RING>::THREADS, 0, s>>>(
-        a, lda, b, ldb, C, ldc, M, N, K, rope, groups);
+        a, lda, b, ldb, C, ldc, M, N, K, ep, groups);
     return hipGetLastError();
 }
 
@@ -760,24 +815,24 @@ hipError_t run_rows(const void* A, int64_t lda, const void* B, int64_t ldb, void
 // N = 37,888: 92 us on tiles against 132 us on the few-row kernel).
 template <Epi EPI>
 hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb, void* C,
-                         int64_t ldc, int M, int N, int K, hipStream_t s, const RopeArgs& rope) {
+                         int64_t ldc, int M, int N, int K, hipStream_t s, const EpiArgs& ep) {
     // the few-row kernel needs whole 32-row slice pairs and K in 128-column stages; RoPE
     // slices pair whole half-heads, so the rotated width and V width split into 32-row groups
     const bool rows_ok = N % 32 == 0 && K % 128 == 0 &&
-                         (EPI != Epi::StoreActRope || (rope.cols % 32 == 0 && (rope.head_dim >> 1) % 16 == 0));
+                         (EPI != Epi::StoreActRope || (ep.cols % 32 == 0 && (ep.head_dim >> 1) % 16 == 0));
     if (M <= 64 && rows_ok) {
-        if (M <= 16) return run_rows<1, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
-        if (M <= 32) return run_rows<2, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
-        return run_rows<4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        if (M <= 16) return run_rows<1, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
+        if (M <= 32) return run_rows<2, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
+        return run_rows<4, EPI>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
     }
     // 65..128 rows against a narrow B: 128 x 128 tiles would leave most CUs idle (N / 128
     // workgroups), so the few-row kernel takes the rows in two 64-row halves, paired on
     // one XCD so each weight slice comes from HBM once.  From N = 32768 (256 tiles, a
     // workgroup per CU) the tiles are faster.
     if (M <= 128 && N < 32768 && rows_ok)
-        return run_rows<4, EPI, true>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        return run_rows<4, EPI, true>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
     if (M <= 128)
-        return run_bf16<128, 128, 32, 64, 64, 4, EPI, 32, 3>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        return run_bf16<128, 128, 32, 64, 64, 4, EPI, 32, 3>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
     // Tile group height (M-tiles per column of the XCD-local block, see tile_coords).  The
     // tiles that finish together store their outputs together: the fewer M-tiles a group
     // spans, the longer the row segments of that store.  Narrow outputs gain from short
@@ -785,10 +840,10 @@ hipError_t dispatch_bf16(const void* A, int64_t lda, const void* B, int64_t ldb,
     // at 262,144 rows: 6.7 ms with groups of 8, 6.0 ms with 2; down 2% faster), while the
     // wide gate/up projection is fastest with 8.
     if constexpr (EPI == Epi::ResidAddF32)
-        return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16, 3, 2>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16, 3, 2>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
     if (N <= 8192)
-        return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16, 3, 4>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
-    return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16, 3, 8>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16, 3, 4>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
+    return run_bf16<256, 256, 32, 128, 64, 4, EPI, 16, 3, 8>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
 }
 
 #endif  // SURR_GEMM_KERNELS_ONLY
@@ -858,7 +913,7 @@ using namespace gemm;
 
 hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, int64_t ldb,
                        void* C, int64_t ldc, int M, int N, int K, hipStream_t s,
-                       const RopeArgs& rope) {
+                       const EpiArgs& ep) {
     if (M <= 0 || N <= 0) return hipSuccess;
     if (t == Act::F32) {
         switch (e) {
@@ -869,13 +924,19 @@ hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, 
         }
     }
     switch (e) {
-        case Epi::StoreAct: return dispatch_bf16<Epi::StoreAct>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
-        case Epi::ResidAddF32: return dispatch_bf16<Epi::ResidAddF32>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
-        case Epi::SwiGLU: return dispatch_bf16<Epi::SwiGLU>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
-        case Epi::StoreF32: return dispatch_bf16<Epi::StoreF32>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+        case Epi::StoreAct: return dispatch_bf16<Epi::StoreAct>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
+        case Epi::ResidAddF32: return dispatch_bf16<Epi::ResidAddF32>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
+        case Epi::SwiGLU: return dispatch_bf16<Epi::SwiGLU>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
+        case Epi::StoreF32: return dispatch_bf16<Epi::StoreF32>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
         case Epi::StoreActRope:
-            if (rope.head_dim != 64 && rope.head_dim != 128) return hipErrorInvalidValue;
-            return dispatch_bf16<Epi::StoreActRope>(A, lda, B, ldb, C, ldc, M, N, K, s, rope);
+            if (ep.head_dim != 64 && ep.head_dim != 128) return hipErrorInvalidValue;
+            return dispatch_bf16<Epi::StoreActRope>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
+        case Epi::LseTile:
+            // records of 128-column tiles for any number of rows (reading the head's weights
+            // once per 128 rows; at 128 rows and more it is the fastest shape measured)
+            if (!ep.head.part || !ep.head.picked || ep.head.n_vid < 0 || ep.head.n_vid > kMaxVerdicts)
+                return hipErrorInvalidValue;
+            return run_bf16<128, 128, 32, 64, 64, 4, Epi::LseTile, 32, 3>(A, lda, B, ldb, C, ldc, M, N, K, s, ep);
     }
     return hipErrorInvalidValue;
 }

@@ -80,6 +80,15 @@ hipError_t launch_append_kv(const uint16_t* qkv, int64_t ld_qkv, int col0, int c
                             const int32_t* len, uint16_t* ck, int64_t ld_ck, int rows,
                             uint16_t* cvt, int64_t ld_c, hipStream_t s);
 
+// Merge the per-tile records of an Epi::LseTile head (n_tiles per row, in tile order) into
+// each row's full-vocabulary log-sum-exp, then, as launch_lse_verdict, the verdict
+// log-probs, their renormalised distribution, its max and first argmax (when nv > 0), and,
+// as launch_lse_next, the first argmax over the vocabulary and the log-prob at the row's
+// target id (each output optional).
+hipError_t launch_lse_combine(const float4* part, int n_tiles, const float* picked, int B, int nv,
+                              float* lp, float* probs, float* conf, int32_t* verdict,
+                              int32_t* next_token, float* target_lp, hipStream_t s);
+
 // Per row of logits: the first argmax over the vocabulary (next_token, optional) and the
 // full-vocabulary log-softmax at target[b] (target_lp, optional).
 hipError_t launch_lse_next(const float* logits, int64_t ld, int B, int V, const int32_t* target,
@@ -128,14 +137,29 @@ hipError_t launch_eval_finalize(const float* speedup, int n, const int32_t* list
                                 double* summary, hipStream_t s);
 
 // ---- k_gemm.hip
-enum class Epi { StoreAct, ResidAddF32, SwiGLU, StoreF32, StoreActRope };
+enum class Epi { StoreAct, ResidAddF32, SwiGLU, StoreF32, StoreActRope, LseTile };
 
-// Rotary embedding applied inside the GEMM epilogue (Epi::StoreActRope): columns
-// [0, cols) hold whole heads of head_dim; within each head, columns i and i + hd/2 of
-// row m rotate by the angle of position pos[m] (table cs[pos][i] = (cos, sin)).  With
-// vt set, columns [cols, N) (the V heads) go transposed to vt[n - cols][vcol[m]]
-// instead of C.
-struct RopeArgs {
+// Full-vocabulary read-out of an LM head inside the GEMM epilogue (Epi::LseTile): the
+// logits never leave the workgroup.  For output row m and column tile t (BN columns) the
+// epilogue writes part[m * n_tiles + t] = (max, sum of exp(z - max), first argmax as int
+// bits, 0) over the tile's valid columns, and copies the logits it holds at the shared
+// ids vid[0 .. n_vid) to picked[m * kPicked + v] and at the row's own id target[m] to
+// picked[m * kPicked + kMaxVerdicts].  launch_lse_combine merges the tiles.
+constexpr int kMaxVerdicts = 16, kPicked = kMaxVerdicts + 1;
+struct HeadArgs {
+    const int32_t* vid = nullptr;     // [n_vid], shared by every row
+    int n_vid = 0;
+    const int32_t* target = nullptr;  // [M] or null
+    float4* part = nullptr;           // [M][n_tiles]
+    float* picked = nullptr;          // [M][kPicked]
+};
+
+// Extra arguments of the fused epilogues.
+// RoPE (Epi::StoreActRope): columns [0, cols) hold whole heads of head_dim; within each
+// head, columns i and i + hd/2 of row m rotate by the angle of position pos[m] (table
+// cs[pos][i] = (cos, sin)).  With vt set, columns [cols, N) (the V heads) go transposed to
+// vt[n - cols][vcol[m]] instead of C.
+struct EpiArgs {
     const int32_t* pos = nullptr;
     const float2* cs = nullptr;
     int cols = 0;
@@ -143,6 +167,7 @@ struct RopeArgs {
     uint16_t* vt = nullptr;
     int64_t ld_vt = 0;
     const int32_t* vcol = nullptr;
+    HeadArgs head;
 };
 
 // C = A[M,K] * B[N,K]^T (both K-contiguous), fp32 accumulation, fused epilogue:
@@ -151,9 +176,10 @@ struct RopeArgs {
 //   SwiGLU      B rows interleave gate/up in 32-row blocks; C[M, N/2] = silu(g) * u
 //   StoreF32    C (fp32) [M, N]
 //   StoreActRope  as StoreAct, with RoPE applied first (bf16 only)
+//   LseTile     per-tile head records (HeadArgs), no C (bf16 only; 128 x 128 tiles)
 hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, int64_t ldb,
                        void* C, int64_t ldc, int M, int N, int K, hipStream_t s,
-                       const RopeArgs& rope = RopeArgs());
+                       const EpiArgs& rope = EpiArgs());
 
 // ---- k_attention.hip
 // Keys and values of shared prompt prefixes, computed once and attended by every prompt
@@ -173,7 +199,7 @@ struct PrefixKV {
 
 // Causal GQA attention over the packed qkv rows.  work[i] = (prompt, q_tile) items;
 // grid = n_items * n_q_heads.  q_tile covers rows [q_tile * attention_q_tile, +tile) of
-// the prompt.  bf16 reads V from the transposed copy vt (see RopeArgs; ld_vt % 8 == 0,
+// the prompt.  bf16 reads V from the transposed copy vt (see EpiArgs; ld_vt % 8 == 0,
 // vt_off[b] % 64 == 0); the fp32 kernel reads V from qkv and ignores vt.  With a prefix
 // (pf != nullptr), every query of prompt b also attends, before its own keys, all
 // pf->len[b] keys of its cached prefix.

@@ -50,7 +50,7 @@ struct LayerW {
 struct WsLayout {
     size_t cu, last, pos_last, vid, work, work_last, vt_off, pfx_len, pfx_off, target, dec_items, dec_first,
         dec_prompt, pos, vcol, x, h, qkv, vt, o, u, gu, o_last, x_last, h_last, u_last, gu_last, y,
-        logits, dec_part, total;
+        logits, head_part, picked, dec_part, total;
     int64_t dec_cap;  // decode-attention slice items the workspace holds (bf16 models)
     int64_t ld_vt;  // columns of the transposed V copy (bf16 models)
 };
@@ -148,7 +148,11 @@ WsLayout layout(const surrogate_model* m, int64_t B, int64_t T) {
     w.u_last = take(e * B * c.d_ff);
     w.gu_last = f32 ? take(4 * B * 2 * c.d_ff) : 0;
     w.y = take(e * B * c.d_model);
-    w.logits = take(4 * B * c.vocab);
+    // LM head: the float32 model writes the logits; bf16 models keep them inside the head
+    // GEMM's workgroups and write per-tile records plus the logits at the ids read out
+    w.logits = f32 ? take(4 * B * c.vocab) : 0;
+    w.head_part = f32 ? 0 : take(16 * B * ((c.vocab + 127) / 128));
+    w.picked = f32 ? 0 : take(4 * B * surr::kPicked);
     w.dec_part = take(4 * (size_t)w.dec_cap * c.n_q_heads * (c.head_dim + 4));
     w.total = off;
     return w;
@@ -186,6 +190,10 @@ surrogate_status check_verdicts(const surrogate_config& c, const int32_t* vid, i
     }
     return SURR_OK;
 }
+
+surrogate_status run_chunks(surrogate_model* m, const int32_t* tokens_d, int64_t row_stride,
+                            const int32_t* lengths_h, int32_t batch, void* workspace_d,
+                            size_t workspace_bytes, const PassIO& io, hipStream_t stream);
 
 surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t row_stride,
                           const int32_t* lengths_h, int32_t batch, void* workspace_d,
@@ -242,8 +250,14 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
     const int max_len = plan.max_len;
     if (reinterpret_cast<uintptr_t>(workspace_d) % kAlign) return fail(SURR_E_INVALID_ARG, "workspace must be 256-byte aligned");
     const WsLayout w = layout(m, batch, T);
-    if (workspace_bytes < w.total)
-        return fail(SURR_E_WORKSPACE, "workspace needs " + std::to_string(w.total) + " bytes");
+    if (workspace_bytes < w.total) {
+        // Token budget: score consecutive chunks of whole prompts, each as large as the
+        // workspace holds (prompts are independent, so every output is unchanged).  A
+        // prefix build lays its cache out per call and is never split.
+        if (io.build || batch == 1)
+            return fail(SURR_E_WORKSPACE, "workspace needs " + std::to_string(w.total) + " bytes");
+        return run_chunks(m, tokens_d, row_stride, lengths_h, batch, workspace_d, workspace_bytes, io, stream);
+    }
     const int32_t n_verdict = io.n_verdict;
     const int32_t* verdict_ids_h = io.verdict_ids_h;
     float* logprobs_d = io.logprobs_d;
@@ -392,7 +406,7 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
         SURR_PHASE_RUN(SURR_PHASE_RMSNORM, surr::launch_rmsnorm(a, x, d, nullptr, T, L.attn_norm, d, c.rms_eps, h, d, stream));
         if (a == Act::BF16) {
             // RoPE on the q and k heads happens in the GEMM epilogue (one rounding)
-            surr::RopeArgs rope;
+            surr::EpiArgs rope;
             rope.pos = d_pos;
             rope.cs = m->rope_cs;
             rope.cols = (nq + nkv) * hd;
@@ -410,12 +424,12 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
             if (!q_last_only) {
                 SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h, d, L.w_qkv, d, qkv, dqkv, Ti, dqkv, d, stream, rope));
             } else {
-                surr::RopeArgs rkv = rope;
+                surr::EpiArgs rkv = rope;
                 rkv.cols = nkv * hd;  // columns [0, nkv hd) of this product are keys
                 const char* w_kv = static_cast<const char*>(L.w_qkv) + 2 * (size_t)dq * d;
                 SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h, d, w_kv, d, static_cast<char*>(qkv) + 2 * (size_t)dq, dqkv, Ti, dqkv - dq, d, stream, rkv));
                 if (!io.build) {
-                    surr::RopeArgs rq;
+                    surr::EpiArgs rq;
                     rq.pos = d_pos_last;
                     rq.cs = m->rope_cs;
                     rq.cols = dq;
@@ -475,11 +489,25 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
     }
     if (io.build) return SURR_OK;
     SURR_PHASE_RUN(SURR_PHASE_LAST_ROWS, surr::launch_rmsnorm(a, x_last, d, nullptr, batch, m->final_norm, d, c.rms_eps, y, d, stream));
-    SURR_PHASE_RUN(SURR_PHASE_LM_HEAD, surr::launch_gemm(a, Epi::StoreF32, y, d, m->lm_head, d, logits, c.vocab, batch, c.vocab, d, stream));
-    if (n_verdict)
-        SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_verdict(logits, c.vocab, batch, c.vocab, d_vid, n_verdict, logprobs_d, probs_d, confidence_d, verdict_d, stream));
-    if (io.next_token_d || io.target_lp_d)
-        SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_next(logits, c.vocab, batch, c.vocab, io.target_ids_h ? d_target : nullptr, io.next_token_d, io.target_ids_h ? io.target_lp_d : nullptr, stream));
+    if (bf16) {
+        // Full-vocabulary read-out without logits in memory: the head GEMM's epilogue
+        // writes per-tile (max, sum of exp, first argmax) records and the logits at the
+        // verdict and target ids; one small kernel merges the tiles in order.
+        surr::EpiArgs hk;
+        hk.head.vid = n_verdict ? d_vid : nullptr;
+        hk.head.n_vid = n_verdict;
+        hk.head.target = io.target_ids_h ? d_target : nullptr;
+        hk.head.part = reinterpret_cast<float4*>(W + w.head_part);
+        hk.head.picked = reinterpret_cast<float*>(W + w.picked);
+        SURR_PHASE_RUN(SURR_PHASE_LM_HEAD, surr::launch_gemm(a, Epi::LseTile, y, d, m->lm_head, d, nullptr, 0, batch, c.vocab, d, stream, hk));
+        SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_combine(hk.head.part, (c.vocab + 127) / 128, hk.head.picked, batch, n_verdict, logprobs_d, probs_d, confidence_d, verdict_d, io.next_token_d, io.target_ids_h ? io.target_lp_d : nullptr, stream));
+    } else {
+        SURR_PHASE_RUN(SURR_PHASE_LM_HEAD, surr::launch_gemm(a, Epi::StoreF32, y, d, m->lm_head, d, logits, c.vocab, batch, c.vocab, d, stream));
+        if (n_verdict)
+            SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_verdict(logits, c.vocab, batch, c.vocab, d_vid, n_verdict, logprobs_d, probs_d, confidence_d, verdict_d, stream));
+        if (io.next_token_d || io.target_lp_d)
+            SURR_PHASE_RUN(SURR_PHASE_LSE_VERDICT, surr::launch_lse_next(logits, c.vocab, batch, c.vocab, io.target_ids_h ? d_target : nullptr, io.next_token_d, io.target_ids_h ? io.target_lp_d : nullptr, stream));
+    }
 #undef SURR_PHASE_RUN
     if (io.append)  // the work above is enqueued: the entries now hold the new tokens
         for (int b = 0; b < batch; ++b) io.append->len[io.prefix_id_h[b]] += lengths_h[b];
@@ -569,6 +597,40 @@ surrogate_status device_scratch(char** out) {
         g_scratch_addr[dev] = static_cast<char*>(p);
     }
     *out = g_scratch_addr[dev];
+    return SURR_OK;
+}
+
+// The batch in consecutive chunks of whole prompts, each the longest run from the current
+// prompt whose workspace fits in workspace_bytes (lengths already checked by the caller).
+surrogate_status run_chunks(surrogate_model* m, const int32_t* tokens_d, int64_t row_stride,
+                            const int32_t* lengths_h, int32_t batch, void* workspace_d,
+                            size_t workspace_bytes, const PassIO& io, hipStream_t stream) {
+    int start = 0;
+    while (start < batch) {
+        int end = start;
+        int64_t t = 0;
+        while (end < batch && layout(m, end - start + 1, t + lengths_h[end]).total <= workspace_bytes)
+            t += lengths_h[end++];
+        if (end == start)
+            return fail(SURR_E_WORKSPACE, "workspace needs " +
+                                              std::to_string(layout(m, 1, lengths_h[start]).total) +
+                                              " bytes for prompt " + std::to_string(start) + " alone");
+        PassIO sub = io;
+        const int nv = io.n_verdict;
+        if (io.prefix_id_h) sub.prefix_id_h = io.prefix_id_h + start;
+        if (io.target_ids_h) sub.target_ids_h = io.target_ids_h + start;
+        if (io.next_token_d) sub.next_token_d = io.next_token_d + start;
+        if (io.target_lp_d) sub.target_lp_d = io.target_lp_d + start;
+        if (io.logprobs_d) sub.logprobs_d = io.logprobs_d + (size_t)start * nv;
+        if (io.probs_d) sub.probs_d = io.probs_d + (size_t)start * nv;
+        if (io.confidence_d) sub.confidence_d = io.confidence_d + start;
+        if (io.verdict_d) sub.verdict_d = io.verdict_d + start;
+        const surrogate_status st = run_pass(m, tokens_d + (int64_t)start * row_stride, row_stride,
+                                             lengths_h + start, end - start, workspace_d,
+                                             workspace_bytes, sub, stream);
+        if (st != SURR_OK) return st;
+        start = end;
+    }
     return SURR_OK;
 }
 

@@ -61,7 +61,18 @@ def run_rows(shape, W, prompts, vid, labels, out_path, meta):
     names = [s[0] for s in synth.tensor_specs(shape)]
     rec = dict(meta, verdict_ids=[int(v) for v in vid], weights_sha256=weights_digest(W, names),
                rows=[])
+    done = {}  # rows a previous, interrupted run already stored for these very inputs
+    if os.path.exists(out_path):
+        with open(out_path) as f:
+            old = json.load(f)
+        if old.get("weights_sha256") == rec["weights_sha256"] and old.get("verdict_ids") == rec["verdict_ids"]:
+            done = {(r["label"], r["length"], r["tokens_sha256"]): r for r in old["rows"]}
     for label, t in zip(labels, prompts):
+        key = (label, int(len(t)), sha(np.asarray(t, np.int32)))
+        if key in done:
+            rec["rows"].append(done[key])
+            print(f"{os.path.basename(out_path)}: {label} kept from the previous run", flush=True)
+            continue
         t0 = time.time()
         r = ot.score(arch, W, [t], vid)
         dt = time.time() - t0

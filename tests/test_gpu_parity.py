@@ -279,3 +279,47 @@ def test_weight_file_model_scores_like_the_tensor_model(tmp_path, name, layers):
         assert torch.equal(a[k], b[k]), k
     if name == "tiny":
         assert_parity(b, oracle_for(shape, W, tok, L, vid), TOL["f32"])
+
+
+# ---------------------------------------------------------------- token budget
+def test_token_budget_chunks_give_the_same_outputs(small3):
+    """A workspace smaller than the batch needs makes the call score consecutive chunks of
+    whole prompts; every output is bitwise the one-pass result.  Below the longest prompt
+    alone the call fails."""
+    shape, scorer, W = small3
+    lengths = [300, 17, 129, 64, 700, 1, 255, 256, 513]
+    tok, L = padded(rng_prompts(shape.vocab, lengths, 29))
+    vid = [3, 4, shape.vocab - 1]
+    whole = scorer.score(tok, L, vid)
+    dtok = torch.from_numpy(tok).to(DEV)
+    alone = B.surrogate_workspace_size(scorer.model, 1, int(L.max()), int(L.max()))
+    third = B.surrogate_workspace_size(scorer.model, 3, 1000, 700)
+    assert alone < third < B.surrogate_workspace_size(scorer.model, len(L), int(L.sum()), int(L.max()))
+    for nbytes in (alone, third):
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+        out = {"logprobs": torch.empty(len(L), len(vid), device=DEV),
+               "p": torch.empty(len(L), len(vid), device=DEV),
+               "confidence": torch.empty(len(L), device=DEV),
+               "verdict": torch.empty(len(L), dtype=torch.int32, device=DEV)}
+        B.surrogate_score_pairs(scorer.model, dtok, L, vid, ws, out["logprobs"], out["confidence"],
+                                out["p"], out["verdict"])
+        for k in whole:
+            assert torch.equal(out[k], whole[k]), (nbytes, k)
+    ws = torch.empty(alone - 256, dtype=torch.uint8, device=DEV)
+    lp, conf = torch.empty(len(L), len(vid), device=DEV), torch.empty(len(L), device=DEV)
+    with pytest.raises(B.SurrogateError) as e:
+        B.surrogate_score_pairs(scorer.model, dtok, L, vid, ws, lp, conf)
+    assert e.value.status == B.SURR_E_WORKSPACE
+
+
+# ---------------------------------------------------------------- fused LM head
+def test_head_read_out_with_a_partial_last_tile():
+    """The LM head's epilogue reduces 128-column tiles; a vocabulary of 4,192 ends in a
+    96-column tile, and verdict ids sit in the first, a middle and that last tile."""
+    shape = synth.ModelShape(n_layers=1, d_model=256, n_q_heads=4, n_kv_heads=2, head_dim=64,
+                             d_ff=512, vocab=4192, max_pos=512)
+    scorer, W = make_scorer(shape, gain_std=0.1, seed=9)
+    tok, L = padded(rng_prompts(shape.vocab, [1, 40, 200, 511], 31))
+    vid = [0, 2100, 4095, 4096, 4191]
+    out = scorer.score(tok, L, vid)
+    assert_parity(out, oracle_for(shape, W, tok, L, vid), TOL["bf16"])
