@@ -34,7 +34,8 @@
 namespace surr {
 namespace {
 
-constexpr int kBQ = 128, kBKV = 64, kStages = 2;
+constexpr int kWaves = 4, kThreads = 64 * kWaves;  // wavefronts of 32 query rows each
+constexpr int kBQ = 32 * kWaves, kBKV = 64, kStages = 2;
 constexpr float kLazy = 8.f;
 
 // 16-byte chunk order inside an LDS row of NCH chunks: XOR with a row function such that
@@ -49,20 +50,21 @@ __device__ __forceinline__ int lds_swz(int row) {
 
 // DMA of 64-key tiles into ring stages.  Position p of a stage holds 16-byte chunk
 // (p % NCH) ^ lds_swz(row) of K row p / NCH, then, for q = p - 64 NCH, chunk
-// (q % 8) ^ lds_swz(d) of V^T row d = q / 8.  Thread tid moves positions i * 256 + tid; its
+// (q % 8) ^ lds_swz(d) of V^T row d = q / 8.  Thread tid moves positions i * kThreads + tid; its
 // byte offsets from the tile's K row k0 and V^T column k0 are fixed, so a tile costs a
 // uniform base and one load per position.  The tile that crosses the prompt's end clamps
 // K rows to the last one (keys past the prompt are masked; V^T columns stay inside the
 // prompt's padded range).
 template <int HD>
 struct AttnDma {
-    static constexpr int NCH = HD / 8, KCH = kBKV * NCH, HALF = KCH / 256;
+    static constexpr int NCH = HD / 8, KCH = kBKV * NCH, HALF = KCH / kThreads;
+    static_assert(KCH % kThreads == 0, "whole loads per thread");
     uint32_t koff[HALF], voff[HALF];
 
     __device__ __forceinline__ AttnDma(int64_t ld, int64_t ld_vt, int tid) {
 #pragma unroll
         for (int i = 0; i < HALF; ++i) {
-            const int p = i * 256 + tid;
+            const int p = i * kThreads + tid;
             const int r = p / NCH, c = (p % NCH) ^ lds_swz<NCH>(r);
             koff[i] = (uint32_t)((r * ld + c * 8) * 2);
             const int d = p >> 3, cv = (p & 7) ^ lds_swz<8>(d);
@@ -78,20 +80,20 @@ struct AttnDma {
         const uint32_t w = stage_lds + (uint32_t)wave * 64u * 16u;
         if (k0 + kBKV <= L) {
 #pragma unroll
-            for (int i = 0; i < HALF; ++i) dma_load_16B_sbase(kb, koff[i], w + i * 256u * 16u);
+            for (int i = 0; i < HALF; ++i) dma_load_16B_sbase(kb, koff[i], w + i * (uint32_t)kThreads * 16u);
         } else {
             const int rmax = L - 1 - k0;
 #pragma unroll
             for (int i = 0; i < HALF; ++i) {
-                const int p = i * 256 + tid;
+                const int p = i * kThreads + tid;
                 const int r = p / NCH, c = (p % NCH) ^ lds_swz<NCH>(r);
                 dma_load_16B_sbase(kb, (uint32_t)((min(r, rmax) * ld + c * 8) * 2),
-                                   w + i * 256u * 16u);
+                                   w + i * (uint32_t)kThreads * 16u);
             }
         }
 #pragma unroll
         for (int i = 0; i < HALF; ++i)
-            dma_load_16B_sbase(vb, voff[i], w + (HALF + i) * 256u * 16u);
+            dma_load_16B_sbase(vb, voff[i], w + (HALF + i) * (uint32_t)kThreads * 16u);
     }
 
     // A tile of a cached prefix: same LDS placement, the cache's own leading dimensions
@@ -104,21 +106,21 @@ struct AttnDma {
         const uint32_t w = stage_lds + (uint32_t)wave * 64u * 16u;
 #pragma unroll
         for (int i = 0; i < HALF; ++i) {
-            const int p = i * 256 + tid;
+            const int p = i * kThreads + tid;
             const int r = p / NCH, c = (p % NCH) ^ lds_swz<NCH>(r);
-            dma_load_16B_sbase(kb, (uint32_t)((r * ld_k + c * 8) * 2), w + i * 256u * 16u);
+            dma_load_16B_sbase(kb, (uint32_t)((r * ld_k + c * 8) * 2), w + i * (uint32_t)kThreads * 16u);
         }
 #pragma unroll
         for (int i = 0; i < HALF; ++i) {
-            const int p = i * 256 + tid;
+            const int p = i * kThreads + tid;
             const int d = p >> 3, cv = (p & 7) ^ lds_swz<8>(d);
-            dma_load_16B_sbase(vb, (uint32_t)((d * ld_v + cv * 8) * 2), w + (HALF + i) * 256u * 16u);
+            dma_load_16B_sbase(vb, (uint32_t)((d * ld_v + cv * 8) * 2), w + (HALF + i) * (uint32_t)kThreads * 16u);
         }
     }
 };
 
 template <int HD, bool PREFIX>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(
+__global__ __launch_bounds__(kThreads, 512 / kThreads) void attn_bf16_kernel(
     const uint16_t* __restrict__ qkv, int64_t ld, const uint16_t* __restrict__ vt, int64_t ld_vt,
     const int32_t* __restrict__ vt_off, uint16_t* __restrict__ out, int64_t ld_out,
     const int32_t* __restrict__ cu, const int2* __restrict__ work, int n_items, int nqh, int nkvh,
@@ -557,7 +559,7 @@ hipError_t launch_attention(Act t, const void* qkv, int64_t ld_qkv, const void* 
                    64 * pk.ld_k * 2 > UINT32_MAX))
             return hipErrorInvalidValue;
 #define SURR_ATTN_BF16(HD, PRE)                                                                 \
-    attn_bf16_kernel<HD, PRE><<<grid, 256, 0, s>>>(q, ld_qkv, v, ld_vt, vt_off, o, ld_out, cu, \
+    attn_bf16_kernel<HD, PRE><<<grid, kThreads, 0, s>>>(q, ld_qkv, v, ld_vt, vt_off, o, ld_out, cu, \
                                                    work, n_items, n_q_heads, n_kv_heads, sl2, pk)
         switch (head_dim) {
             case 64: if (pf) SURR_ATTN_BF16(64, true); else SURR_ATTN_BF16(64, false); break;

@@ -15,16 +15,17 @@ residual stream).  Nothing else is rounded.  Its error against the exact float64
 is therefore the error that the bf16 storage by itself causes: a kernel with these
 storage types cannot do better, whatever its summation order.
 
-A single run gives one sample of that error.  A different summation order changes
-float32 values in their last bits and so flips some bf16 roundings, and the path's own
-choices (the scale of the unnormalised attention probabilities, say) round other values
-altogether, so two correct bf16 paths differ from the exact result by different draws of
-the same size.  ``members`` selects an ensemble of such draws: member 0 rounds the exact
-values to nearest even; member k > 0 rounds every value on a scaled bf16 grid, bf16(x s)/s,
-with a factor s = 2^u, u uniform in [0, 1) per value, from a generator seeded with k.
-Floating-point grids are invariant under scaling by a power of two, so the relative
-rounding error keeps its distribution (at most 2^-8, a CPU test pins its rms to plain
-rounding's) while its value for each element becomes an independent draw.
+A single run gives one sample of that error.  Another correct bf16 path rounds the same
+values at the same points, so the structured part of the error (which way a given value
+rounds) is shared; it differs in float32 noise (summation order, a hardware exp), which
+flips the roundings of values that lie near a rounding boundary, and in the scale at which
+it rounds the attention probabilities: the kernel keeps them relative to a running maximum
+that it updates lazily, i.e. multiplied by a per-row factor that is not a power of two.
+``members`` selects an ensemble of such runs: member 0 rounds the exact values to nearest
+even; member k > 0, from a generator seeded with k, first multiplies every value it rounds
+by (1 + 2^-16 u) with u uniform in [-1, 1) (float32-sized noise; the roundings stay
+nearest-even), and rounds each row of attention probabilities at a scale 2^v, v uniform in
+[0, 1) per row (the rounded row is divided by the scale again).
 
 With ``rounding=False`` the module computes the exact forward; a CPU test pins that mode
 to the float64 oracle.
@@ -35,6 +36,8 @@ import math
 
 import numpy as np
 import torch
+
+PERTURB = 2.0 ** -16
 
 
 
@@ -61,14 +64,22 @@ class _Rounder:
     def _rne(x):
         return x.to(torch.float32).to(torch.bfloat16).to(torch.float64)
 
+    def _uniform(self, shape, device):
+        return torch.rand(shape, generator=self.gen, device=device, dtype=torch.float64)
+
     def bf16(self, x):
         if not self.rounding:
             return x
         if self.gen is None:
             return self._rne(x)
-        u = torch.rand(x.shape, generator=self.gen, device=x.device, dtype=torch.float64)
-        scale = torch.exp2(u)
-        return self._rne(x * scale) / scale
+        return self._rne(x * (1.0 + PERTURB * (2.0 * self._uniform(x.shape, x.device) - 1.0)))
+
+    def bf16_rows(self, p):
+        """Attention probabilities p[rows, keys], each row rounded at its own scale."""
+        if not self.rounding or self.gen is None:
+            return self.bf16(p)
+        scale = torch.exp2(self._uniform((p.shape[0], 1), p.device))
+        return self.bf16(p * scale) / scale
 
     def f32(self, x):
         if not self.rounding:
@@ -104,7 +115,7 @@ def _attention(q, k, v, R):
         s.masked_fill_(future, -math.inf)
         pf = torch.exp(s - s.amax(dim=1, keepdim=True))
         l = pf.sum(dim=1, keepdim=True)
-        o[:, a, :] = (R.bf16(pf) @ v[:, c, :].contiguous()) / l
+        o[:, a, :] = (R.bf16_rows(pf) @ v[:, c, :].contiguous()) / l
         del s, pf
     return o
 

@@ -156,3 +156,37 @@ def test_14b_shape_full_width_reduced_depth():
     ref = rows_of(ot.score(arch_of(shape), W, prompts, vid))
     emu = emulate(shape, W, prompts, vid)
     assert_parity_floor(out, range(len(L)), ref, emu)
+
+
+@pytest.mark.timeout(900)
+def test_1p5b_error_statistics_match_the_bf16_storage_floor():
+    """Over a whole batch the HIP path's rounding error must look like the bf16 storage
+    floor, not just stay below a bound per prompt: a path with a systematic extra error
+    (a value stored at lower precision, a lossy exp) would pass the per-prompt bars yet
+    shift this statistic.  The full 1.5B-shape batch (64 prompts, 28 layers, 5 verdicts:
+    320 log-probs); the reference is the emulation's exact float64 forward on the GPU
+    (pinned to the oracle's forward on the CPU), against which both the HIP path and four
+    independent emulation members (storage roundings only) are measured.  The HIP error's
+    rms must lie within 25% of the members' (1,280 values) and its largest value within
+    the members' largest plus 25%."""
+    from bf16_emulation import Bf16Emulation
+    w = synth.CONFIGS["1p5b"]
+    scorer, W = make_scorer(w.shape)
+    tok, L = synth.make_prompts(w)
+    vid = synth.verdict_ids(w)
+    out = scorer.score(tok, L, vid)
+    lp_hip = out["logprobs"].cpu().numpy().astype(np.float64)
+    del scorer
+    torch.cuda.empty_cache()
+    prompts = [tok[i, : L[i]] for i in range(len(L))]
+    arch = arch_of(w.shape)
+    exact = Bf16Emulation(arch, W, "cuda:0", rounding=False).score(prompts, vid, progress=True)
+    members = Bf16Emulation(arch, W, "cuda:0").score(prompts, vid, members=(1, 2, 3, 4), progress=True)
+    e_hip = lp_hip - exact["logprobs"][0]
+    e_emu = members["logprobs"] - exact["logprobs"][0][None]
+    r_hip, r_emu = float(np.sqrt((e_hip ** 2).mean())), float(np.sqrt((e_emu ** 2).mean()))
+    m_hip, m_emu = float(np.abs(e_hip).max()), float(np.abs(e_emu).max())
+    print(f"1.5B batch log-prob error: HIP rms {r_hip:.3e} max {m_hip:.3e}; storage-floor "
+          f"members rms {r_emu:.3e} max {m_emu:.3e} (ratio of rms {r_hip / r_emu:.3f})", flush=True)
+    assert r_hip <= 1.25 * r_emu
+    assert m_hip <= 1.25 * m_emu
