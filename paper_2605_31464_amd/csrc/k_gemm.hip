@@ -110,6 +110,9 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
                                                         EpiArgs ep) {
     using S = Tile<BM, BN, BK, WM, WN, NST, MF>;
     using Acc = typename std::conditional<MF == 32, f32x16, f32x4>::type;
+    // SwiGLU pairs the gate fragment j of a wavefront with its up fragment 32 columns on,
+    // so a wavefront's columns must hold whole 64-column gate/up block pairs
+    static_assert(EPI != Epi::SwiGLU || WN % 64 == 0, "SwiGLU needs wavefront tiles of whole gate/up pairs");
     __shared__ uint4 lds[NST * S::STAGE];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / S::WAVES_N, wn = wave % S::WAVES_N;
