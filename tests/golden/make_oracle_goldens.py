@@ -16,7 +16,10 @@ Cases:
   workload (8,417 to 15,979 tokens), and one prompt of max_pos = 16,384 tokens (tokens
   from seed 3).
 
-Usage: python tests/golden/make_oracle_goldens.py [7b] [14b]   (default: both)
+Usage: python tests/golden/make_oracle_goldens.py [7b] [14b] [--only "prompt 1,longest"]
+(default: both cases, every row; --only computes the rows whose labels start with the
+given prefixes; rows already stored for the same inputs are kept, and each write merges
+with what another run stored meanwhile).
 """
 from __future__ import annotations
 
@@ -56,6 +59,26 @@ def weights_digest(W, names) -> str:
     return h.hexdigest()
 
 
+def write_merged(out_path, rec, labels):
+    """Write rec after merging in the rows another run stored for the same inputs (two
+    runs may share the rows of one case), in the case's row order."""
+    rows = {r["label"]: r for r in rec["rows"]}
+    if os.path.exists(out_path):
+        with open(out_path) as f:
+            old = json.load(f)
+        if old.get("weights_sha256") == rec["weights_sha256"]:
+            for r in old["rows"]:
+                rows.setdefault(r["label"], r)
+    out = dict(rec, rows=[rows[l] for l in labels if l in rows])
+    tmp = out_path + ".tmp"
+    with open(tmp, "w") as f:
+        json.dump(out, f, indent=1)
+    os.replace(tmp, out_path)
+
+
+ONLY = None  # labels (prefixes) to compute in this run, None for all
+
+
 def run_rows(shape, W, prompts, vid, labels, out_path, meta):
     arch = arch_of(shape)
     names = [s[0] for s in synth.tensor_specs(shape)]
@@ -68,6 +91,8 @@ def run_rows(shape, W, prompts, vid, labels, out_path, meta):
         if old.get("weights_sha256") == rec["weights_sha256"] and old.get("verdict_ids") == rec["verdict_ids"]:
             done = {(r["label"], r["length"], r["tokens_sha256"]): r for r in old["rows"]}
     for label, t in zip(labels, prompts):
+        if ONLY is not None and not any(label.startswith(o) for o in ONLY):
+            continue
         key = (label, int(len(t)), sha(np.asarray(t, np.int32)))
         if key in done:
             rec["rows"].append(done[key])
@@ -83,8 +108,7 @@ def run_rows(shape, W, prompts, vid, labels, out_path, meta):
             margin=float(r["margin"][0]), oracle_seconds=round(dt, 1)))
         print(f"{os.path.basename(out_path)}: {label} (L={len(t)}) done in {dt:.0f} s "
               f"lp={r['logprobs'][0]}", flush=True)
-        with open(out_path, "w") as f:  # written after every row
-            json.dump(rec, f, indent=1)
+        write_merged(out_path, rec, labels)
 
 
 def case_7b():
@@ -119,6 +143,11 @@ def case_14b():
 
 
 if __name__ == "__main__":
-    which = sys.argv[1:] or ["7b", "14b"]
+    args = sys.argv[1:]
+    if "--only" in args:  # e.g. --only "prompt 1,shortest"
+        i = args.index("--only")
+        ONLY = [o.strip() for o in args[i + 1].split(",")]
+        del args[i: i + 2]
+    which = args or ["7b", "14b"]
     for c in which:
         {"7b": case_7b, "14b": case_14b}[c]()
