@@ -153,3 +153,36 @@ def test_7b_shared_prefix_workload_matches_oracle_and_plain_path():
     one = {k: v[:, :1] for k, v in emu.items()}
     assert_parity_floor(out, [i], ref, one, [f"prefix path, candidate {i}"])
     assert_parity_floor(plain, [i], ref, one, [f"plain path, candidate {i}"])
+
+
+def test_token_budget_chunks_of_suffixes_and_cache_appends():
+    """Chunked calls (a workspace for the longest prompt alone) give bitwise the one-pass
+    outputs: suffix scoring against cached prefixes (prefix ids and outputs offset per
+    chunk) and appends to cache entries with greedy and teacher-forced read-outs."""
+    shape = synth.CONFIGS["1p5b"].shape.replace(n_layers=2)
+    scorer, W = make_scorer(shape)
+    ptok, Lp = padded(rng_prompts(shape.vocab, [90, 200, 64], 57))
+    stok, Ls = padded(rng_prompts(shape.vocab, [17, 300, 64, 129, 250, 1], 58))
+    pid = np.array([1, 0, -1, 2, 1, 0], np.int32)
+    vid = [shape.vocab - 2, shape.vocab - 1]
+    cache = scorer.build_prefixes(ptok, Lp)
+    whole = scorer.score_suffixes(cache, pid, stok, Ls, vid)
+    dtok = torch.from_numpy(stok).to("cuda:0")
+    small = B.surrogate_workspace_size(scorer.model, 1, int(Ls.max()), int(Ls.max()))
+    ws = torch.empty(small, dtype=torch.uint8, device="cuda:0")
+    out = {k: torch.empty_like(v) for k, v in whole.items()}
+    B.surrogate_score_suffixes(scorer.model, cache, pid, dtok, Ls, vid, ws, out["logprobs"],
+                               out["confidence"], out["p"], out["verdict"])
+    for k in whole:
+        assert torch.equal(out[k], whole[k]), k
+    # appends: two caches of the same entries, one filled in one pass, one in chunks
+    caps = [512] * len(Ls)
+    targets = [3, 5, 7, 11, 13, 17]
+    c1, c2 = scorer.create_cache(caps), scorer.create_cache(caps)
+    eids = list(range(len(Ls)))
+    n1, t1 = scorer.extend(c1, eids, stok, Ls, targets)
+    n2 = torch.empty_like(n1)
+    t2 = torch.empty_like(t1)
+    B.surrogate_cache_extend(scorer.model, c2, eids, dtok, Ls, ws, targets, n2, t2)
+    assert torch.equal(n1, n2) and torch.equal(t1, t2)
+    assert B.surrogate_cache_lengths(c2, len(Ls)).tolist() == Ls.tolist()
