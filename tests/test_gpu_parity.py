@@ -323,3 +323,23 @@ def test_head_read_out_with_a_partial_last_tile():
     vid = [0, 2100, 4095, 4096, 4191]
     out = scorer.score(tok, L, vid)
     assert_parity(out, oracle_for(shape, W, tok, L, vid), TOL["bf16"])
+
+
+def test_head_read_out_over_more_than_128_rows():
+    """200 prompts: the LM head's records span two 128-row tiles; every row's outputs equal
+    those of the same prompt scored in a batch of 7, and sampled rows match the oracle."""
+    shape = synth.CONFIGS["small"].shape.replace(n_layers=2)
+    scorer, W = make_scorer(shape, gain_std=0.1, seed=11)
+    rng = np.random.default_rng(37)
+    lengths = rng.integers(1, 160, 200)
+    prompts = rng_prompts(shape.vocab, lengths, 38)
+    tok, L = padded(prompts)
+    vid = [1, shape.vocab - 1]
+    out = scorer.score(tok, L, vid)
+    for s0 in range(0, 200, 7):
+        t7, l7 = padded(prompts[s0: s0 + 7])
+        part = scorer.score(t7, l7, vid)
+        for k in out:
+            assert torch.equal(part[k], out[k][s0: s0 + 7]), (s0, k)
+    rows = [0, 127, 128, 199]
+    assert_parity(out, oracle_for(shape, W, tok, L, vid, rows), TOL["bf16"], rows)
