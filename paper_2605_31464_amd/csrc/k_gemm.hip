@@ -13,6 +13,7 @@
 //
 // Few-row path (decode steps, last-position rows): gemm_rows_kernel below.
 // fp32 path: a plain LDS-tiled FMA kernel for the float32 model.
+#include <algorithm>
 #include <climits>
 #include <type_traits>
 
@@ -124,12 +125,17 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
 
     // Direct-to-LDS loads: wavefront `wave`, load j fills the 64 consecutive slots
     // (wave * LOADS + j) * 64 + lane of a stage (the hardware places lane l's 16 bytes at
-    // slot base + l).  Slot -> (row, physical chunk) -> logical chunk via the swizzle;
-    // rows past M or N are clamped (their results are never stored).  Each load reads
-    // either the A tile or the B tile (uniform per wavefront and load), so a thread keeps
-    // only a 32-bit byte offset per load against the tile's base pointer.
+    // slot base + l), i.e. 16 rows x 4 chunks.  Slot -> (row, physical chunk) -> logical
+    // chunk via the swizzle; rows past M or N are clamped (their results are never
+    // stored).  B is panel-packed: the 16 rows of a load are 1 KB of consecutive bytes of
+    // one block, and a stage k0 further sits k0 * kPanel values on in every panel; a tile
+    // may span two panels when b_row0 is not a multiple of BN.  Each load reads either
+    // the A tile or the B tile (uniform per wavefront and load), so a thread keeps only a
+    // 32-bit byte offset per load against the tile's base pointer.
+    static_assert(BK == 32, "panel blocks are 32 columns wide");
+    const int64_t nb = (int64_t)ep.b_row0 + n0;  // first weight row of the tile
     const char* a_tile = reinterpret_cast<const char*>(A + (int64_t)m0 * lda);
-    const char* b_tile = reinterpret_cast<const char*>(B + (int64_t)n0 * ldb);
+    const char* b_tile = reinterpret_cast<const char*>(B + (nb / kPanel) * kPanel * K + (nb % kPanel) * 32);
     uint32_t goff[S::LOADS];
     const uint32_t lds_base = lds_offset(lds);
 #pragma unroll
@@ -141,12 +147,14 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64, MINB) void gemm_bf16_ke
         } else {
             const int sb = slot - S::A_SLOTS;
             const int r = sb / S::CH, c = (sb % S::CH) ^ swz<S::CH, SWZ>(r);
-            goff[j] = (uint32_t)(((int64_t)(min(n0 + r, N - 1) - n0) * ldb + c * 8) * 2);
+            const int64_t q = (int64_t)ep.b_row0 + min(n0 + r, N - 1);
+            goff[j] = (uint32_t)(((q / kPanel - nb / kPanel) * kPanel * K + (q % kPanel - nb % kPanel) * 32 + c * 8) * 2);
         }
     }
     // Source of load j of this thread for the stage starting at column k0.
 #define SURR_DMA_SRC(j, k0)                                                                  \
-    ((((wave * S::LOADS + (j)) * 64) < S::A_SLOTS ? a_tile : b_tile) + 2 * (int64_t)(k0) + goff[j])
+    ((((wave * S::LOADS + (j)) * 64) < S::A_SLOTS ? a_tile + 2 * (int64_t)(k0)                   \
+                                                  : b_tile + 2 * (int64_t)(k0) * kPanel) + goff[j])
 
     // One stage of direct-to-LDS loads: load j of wavefront `wave` fills the 64 slots
     // starting at (wave * LOADS + j) * 64.
@@ -640,20 +648,27 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restri
     int slice[NF];
 #pragma unroll
     for (int f = 0; f < NF; ++f) slice[f] = rows_slice<NF, EPI>(g, f, ep);
-    const char* b_base = reinterpret_cast<const char*>(B + (int64_t)slice[0] * ldb);
-    const char* a_base = reinterpret_cast<const char*>(A);
     // Load j of this thread fills slot (wave * LOADS + j) * 64 + lane of a stage: slots
-    // [0, ROWS_B * CH) hold the B slices, the rest the A rows; the chunk order inside a
-    // row is XOR-swizzled with the row's low 4 bits (16 rows read at one logical chunk
-    // hit 16 distinct bank groups).  Offsets are relative to b_base / a_base.
+    // [0, ROWS_B * CH) hold the B slices, the rest the A rows.  B (panel-packed) is kept
+    // block-major in LDS as in HBM: slot (b * ROWS_B + r) * 4 + (c ^ ((r >> 2) & 3)) holds
+    // chunk c of the stage's 32-column block b for slice row r, so a load copies one
+    // 1 KB run (16 rows of one block) and the 16 rows that one fragment read takes at a
+    // chunk hit 16 distinct bank groups.  A rows are row-major, the chunk order inside a
+    // row XOR-swizzled with the row's low 4 bits.  Offsets are relative to b_base (the
+    // panel of the first slice row) and a_base.
+    const int64_t q0 = (int64_t)ep.b_row0 + slice[0];
+    const char* b_base = reinterpret_cast<const char*>(B + (q0 / kPanel) * kPanel * K);
+    const char* a_base = reinterpret_cast<const char*>(A);
     uint32_t goff[R::LOADS];
 #pragma unroll
     for (int j = 0; j < R::LOADS; ++j) {
         const int slot = (wave * R::LOADS + j) * 64 + lane;
         if (slot < R::ROWS_B * R::CH) {
-            const int r = slot / R::CH, c = (slot % R::CH) ^ (r & 15);
-            const int row = min(slice[r >> 4] + (r & 15), N - 1) - slice[0];
-            goff[j] = (uint32_t)(((int64_t)row * ldb + c * 8) * 2);
+            const int b = slot / (R::ROWS_B * 4), r = (slot / 4) % R::ROWS_B;
+            const int c = (slot % 4) ^ ((r >> 2) & 3);
+            const int64_t q = (int64_t)ep.b_row0 + min(slice[r >> 4] + (r & 15), N - 1);
+            goff[j] = (uint32_t)(((q / kPanel - q0 / kPanel) * kPanel * K + (int64_t)b * kPanel * 32 +
+                                  (q % kPanel) * 32 + c * 8) * 2);
         } else {
             const int sa = slot - R::ROWS_B * R::CH;
             const int r = sa / R::CH, c = (sa % R::CH) ^ (r & 15);
@@ -665,7 +680,7 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restri
 #pragma unroll
         for (int j = 0; j < R::LOADS; ++j) {
             const bool is_b = (wave * R::LOADS + j) * 64 < R::ROWS_B * R::CH;
-            dma_load_16B((is_b ? b_base : a_base) + 2 * (int64_t)k0 + goff[j],
+            dma_load_16B((is_b ? b_base + 2 * (int64_t)k0 * kPanel : a_base + 2 * (int64_t)k0) + goff[j],
                          lds_base + (uint32_t)((stage * R::STAGE + (wave * R::LOADS + j) * 64) * 16));
         }
     };
@@ -689,7 +704,7 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(const uint16_t* __restri
 #pragma unroll
                 for (int f = 0; f < NF; ++f) {
                     const int r = 16 * f + rb;
-                    fw[f] = __builtin_bit_cast(bf16x8, L[r * R::CH + (c ^ (r & 15))]);
+                    fw[f] = __builtin_bit_cast(bf16x8, L[(s * R::ROWS_B + r) * 4 + (ck ^ ((r >> 2) & 3))]);
                 }
                 const int ra = 16 * wave + rb;
                 const bf16x8 fx = __builtin_bit_cast(bf16x8, L[R::ROWS_B * R::CH + ra * R::CH + (c ^ (ra & 15))]);
@@ -913,6 +928,30 @@ hipError_t run_f32(const void* A, int64_t lda, const void* B, int64_t ldb, void*
 
 #ifndef SURR_GEMM_KERNELS_ONLY
 using namespace gemm;
+
+// One 16-byte chunk (8 values) of the packed matrix per thread.
+__global__ __launch_bounds__(256) void pack_panels_kernel(const uint4* __restrict__ src, int64_t rows,
+                                                          int64_t K, uint4* __restrict__ dst,
+                                                          int64_t chunks) {
+    const int64_t per_panel = (int64_t)kPanel * K / 8;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < chunks;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t p = i / per_panel, rem = i % per_panel;
+        const int64_t blk = rem / (kPanel * 4), r = (rem / 4) % kPanel, c = rem % 4;
+        const int64_t n = p * kPanel + r;
+        dst[i] = n < rows ? src[(n * K + blk * 32 + c * 8) / 8] : make_uint4(0, 0, 0, 0);
+    }
+}
+
+hipError_t launch_pack_panels(const uint16_t* src, int64_t rows, int64_t K, uint16_t* dst,
+                              hipStream_t s) {
+    if (rows <= 0 || K <= 0 || K % 32) return hipErrorInvalidValue;
+    const int64_t chunks = packed_rows(rows) * K / 8;
+    const int64_t blocks = std::min<int64_t>((chunks + 255) / 256, 65536);
+    pack_panels_kernel<<<(unsigned)blocks, 256, 0, s>>>(reinterpret_cast<const uint4*>(src), rows, K,
+                                                        reinterpret_cast<uint4*>(dst), chunks);
+    return hipGetLastError();
+}
 
 hipError_t launch_gemm(Act t, Epi e, const void* A, int64_t lda, const void* B, int64_t ldb,
                        void* C, int64_t ldc, int M, int N, int K, hipStream_t s,

@@ -168,9 +168,25 @@ struct EpiArgs {
     int64_t ld_vt = 0;
     const int32_t* vcol = nullptr;
     HeadArgs head;
+    int b_row0 = 0;  // bf16: first row of B inside its packed matrix (a multiple of 16)
 };
 
-// C = A[M,K] * B[N,K]^T (both K-contiguous), fp32 accumulation, fused epilogue:
+// Layout of every bf16 weight matrix W [N, K] (K a multiple of 32), written once at load
+// time: panels of kPanel rows, each panel K / 32 consecutive blocks of kPanel x 32 values
+// (row-major inside a block); rows past N are zero.  Element (n, k) sits at
+//   (n / kPanel) * kPanel * K + (k / 32) * kPanel * 32 + (n % kPanel) * 32 + k % 32.
+// Sixteen consecutive rows of one 32-column block are 1 KB of consecutive bytes, which is
+// what one wavefront's direct-to-LDS load reads.
+constexpr int kPanel = 256;
+inline int64_t packed_rows(int64_t n) { return (n + kPanel - 1) / kPanel * kPanel; }
+// dst [packed_rows(rows) * K] <- src [rows][K] (row-major, K-contiguous)
+hipError_t launch_pack_panels(const uint16_t* src, int64_t rows, int64_t K, uint16_t* dst,
+                              hipStream_t s);
+
+// C = A[M,K] * B[N,K]^T, fp32 accumulation, fused epilogue.  A is row-major (lda); for
+// fp32 models B is row-major too (ldb), for bf16 models B is a panel-packed weight matrix
+// (above) whose rows [rope.b_row0, rope.b_row0 + N) are the operand (ldb unused).
+// Epilogues:
 //   StoreAct    C (activation type) [M, N]
 //   ResidAddF32 C (fp32) += result
 //   SwiGLU      B rows interleave gate/up in 32-row blocks; C[M, N/2] = silu(g) * u

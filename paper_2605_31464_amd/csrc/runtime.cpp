@@ -426,8 +426,8 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
             } else {
                 surr::EpiArgs rkv = rope;
                 rkv.cols = nkv * hd;  // columns [0, nkv hd) of this product are keys
-                const char* w_kv = static_cast<const char*>(L.w_qkv) + 2 * (size_t)dq * d;
-                SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h, d, w_kv, d, static_cast<char*>(qkv) + 2 * (size_t)dq, dqkv, Ti, dqkv - dq, d, stream, rkv));
+                rkv.b_row0 = (int)dq;  // the K and V rows of the packed w_qkv
+                SURR_PHASE_RUN(SURR_PHASE_GEMM_QKV, surr::launch_gemm(a, Epi::StoreActRope, h, d, L.w_qkv, d, static_cast<char*>(qkv) + 2 * (size_t)dq, dqkv, Ti, dqkv - dq, d, stream, rkv));
                 if (!io.build) {
                     surr::EpiArgs rq;
                     rq.pos = d_pos_last;
@@ -688,7 +688,10 @@ surrogate_status surrogate_load_weights_tensors(const surrogate_config* cfg, con
     const size_t e = m->esz, d = c.d_model, ff = c.d_ff, V = c.vocab;
     const size_t dq = m->d_q(), dkv = m->d_kv(), half = c.head_dim / 2;
 
-    // Arena: embed, layers, final norm, head, RoPE table, error word.
+    // Arena: embed, layers, final norm, head, RoPE table, error word.  bf16 projection
+    // matrices are stored panel-packed (rows padded to whole panels).
+    const bool packed = m->act == Act::BF16;
+    auto mat = [&](size_t rows, size_t k) { return (packed ? (size_t)surr::packed_rows((int64_t)rows) : rows) * k * e; };
     size_t off = 0;
     auto take = [&](size_t bytes) { size_t o = off; off += align_up(bytes); return o; };
     const size_t o_embed = take(V * d * e);
@@ -696,13 +699,13 @@ surrogate_status surrogate_load_weights_tensors(const surrogate_config* cfg, con
     std::vector<LOff> lo(c.n_layers);
     for (auto& l : lo) {
         l.an = take(4 * d);
-        l.qkv = take((dq + 2 * dkv) * d * e);
-        l.o = take(d * dq * e);
+        l.qkv = take(mat(dq + 2 * dkv, d));
+        l.o = take(mat(d, dq));
         l.mn = take(4 * d);
-        l.gu = take(2 * ff * d * e);
-        l.dn = take(d * ff * e);
+        l.gu = take(mat(2 * ff, d));
+        l.dn = take(mat(d, ff));
     }
-    const size_t o_fn = take(4 * d), o_head = take(V * d * e);
+    const size_t o_fn = take(4 * d), o_head = take(mat(V, d));
     const size_t o_rope = take((size_t)c.max_pos * half * sizeof(float2)), o_err = take(4);
     if (hipMalloc(&m->arena, off) != hipSuccess) {
         surrogate_free(m);
@@ -720,31 +723,52 @@ surrogate_status surrogate_load_weights_tensors(const surrogate_config* cfg, con
 
     const hipMemcpyKind kind = tensors_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
     std::vector<float2> cs((size_t)c.max_pos * half);
+    // bf16 matrices are first assembled row-major in a staging buffer (the largest one's
+    // size, freed when loading ends), then packed into the arena; fp32 ones go straight in.
+    char* stage = nullptr;
     auto body = [&]() -> surrogate_status {
         auto cp = [&](void* dst, const void* src, size_t bytes) {
             return hipMemcpyAsync(dst, src, bytes, kind, stream);
         };
+        if (packed) {
+            const size_t most = std::max({(dq + 2 * dkv) * d, d * dq, 2 * ff * d, d * ff, V * d}) * e;
+            if (hipMalloc(&stage, most) != hipSuccess)
+                return fail(SURR_E_OOM, "weight staging buffer of " + std::to_string(most) + " bytes");
+        }
+        // matrix [rows, k] assembled at `rm` (row-major) by fill(rm), then placed at dst
+        auto put = [&](void* dst, size_t rows, size_t k, auto fill) -> hipError_t {
+            char* rm = packed ? stage : static_cast<char*>(dst);
+            hipError_t err = fill(rm);
+            if (err == hipSuccess && packed)
+                err = surr::launch_pack_panels(reinterpret_cast<const uint16_t*>(rm), (int64_t)rows, (int64_t)k,
+                                               static_cast<uint16_t*>(dst), stream);
+            return err;
+        };
         SURR_HIP(cp(m->embed, tensors[0], V * d * e));
         for (int l = 0; l < c.n_layers; ++l) {
             const void* const* t = tensors + 1 + 9 * l;
-            char* qkv = static_cast<char*>(m->layers[l].w_qkv);
             SURR_HIP(cp(m->layers[l].attn_norm, t[0], 4 * d));
-            SURR_HIP(cp(qkv, t[1], dq * d * e));
-            SURR_HIP(cp(qkv + dq * d * e, t[2], dkv * d * e));
-            SURR_HIP(cp(qkv + (dq + dkv) * d * e, t[3], dkv * d * e));
-            SURR_HIP(cp(m->layers[l].w_o, t[4], d * dq * e));
+            SURR_HIP(put(m->layers[l].w_qkv, dq + 2 * dkv, d, [&](char* qkv) {
+                hipError_t err = cp(qkv, t[1], dq * d * e);
+                if (err == hipSuccess) err = cp(qkv + dq * d * e, t[2], dkv * d * e);
+                if (err == hipSuccess) err = cp(qkv + (dq + dkv) * d * e, t[3], dkv * d * e);
+                return err;
+            }));
+            SURR_HIP(put(m->layers[l].w_o, d, dq, [&](char* w) { return cp(w, t[4], d * dq * e); }));
             SURR_HIP(cp(m->layers[l].mlp_norm, t[5], 4 * d));
             // gate/up interleave: block p of 32 gate rows goes to rows [64p, 64p+32), the
             // matching up rows to [64p+32, 64p+64).
-            const size_t blk = 32 * d * e;
-            char* gu = static_cast<char*>(m->layers[l].w_gu);
-            SURR_HIP(hipMemcpy2DAsync(gu, 2 * blk, t[6], blk, blk, ff / 32, kind, stream));
-            SURR_HIP(hipMemcpy2DAsync(gu + blk, 2 * blk, t[7], blk, blk, ff / 32, kind, stream));
-            SURR_HIP(cp(m->layers[l].w_down, t[8], d * ff * e));
+            SURR_HIP(put(m->layers[l].w_gu, 2 * ff, d, [&](char* gu) {
+                const size_t blk = 32 * d * e;
+                hipError_t err = hipMemcpy2DAsync(gu, 2 * blk, t[6], blk, blk, ff / 32, kind, stream);
+                if (err == hipSuccess) err = hipMemcpy2DAsync(gu + blk, 2 * blk, t[7], blk, blk, ff / 32, kind, stream);
+                return err;
+            }));
+            SURR_HIP(put(m->layers[l].w_down, d, ff, [&](char* w) { return cp(w, t[8], d * ff * e); }));
         }
         const int last = 1 + 9 * c.n_layers;
         SURR_HIP(cp(m->final_norm, tensors[last], 4 * d));
-        SURR_HIP(cp(m->lm_head, tensors[last + 1], V * d * e));
+        SURR_HIP(put(m->lm_head, V, d, [&](char* w) { return cp(w, tensors[last + 1], V * d * e); }));
         // RoPE: theta = pos * base^(-2i/hd) in float64, stored as float32 (cos, sin).
         for (int p = 0; p < c.max_pos; ++p)
             for (size_t i = 0; i < half; ++i) {
@@ -759,6 +783,10 @@ surrogate_status surrogate_load_weights_tensors(const surrogate_config* cfg, con
         return SURR_OK;
     };
     const surrogate_status st = body();
+    if (stage) {
+        hipStreamSynchronize(stream);
+        hipFree(stage);
+    }
     if (st != SURR_OK) {
         hipStreamSynchronize(stream);
         surrogate_free(m);
