@@ -25,6 +25,13 @@
  *    argument errors are reported synchronously and then nothing is enqueued.
  *  - A model handle is read-only after loading; concurrent calls on one handle are
  *    allowed only with distinct workspaces and output buffers.
+ *  - A call that fails after it took device memory releases it before returning, and a
+ *    failed scoring, prefix or cache call leaves the model and its caches as they were
+ *    (a failed cache_extend leaves its entries at their previous lengths).  For testing
+ *    these paths, the environment variable SURROGATE_FAULT=alloc:N makes the N-th device
+ *    or pinned allocation fail (SURR_E_OOM) and SURROGATE_FAULT=launch:N the N-th checked
+ *    HIP call (SURR_E_HIP), counted from when the variable took its value; the calls
+ *    that load weights, build prefixes, create caches or run a pass re-read it.
  */
 #ifndef SURROGATE_H
 #define SURROGATE_H

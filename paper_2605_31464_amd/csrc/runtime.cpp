@@ -4,7 +4,9 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <numeric>
@@ -27,9 +29,45 @@ surrogate_status fail(surrogate_status s, const std::string& msg) {
     return s;
 }
 
+// Fault injection for the cleanup paths, forced from the host.  SURROGATE_FAULT=alloc:N
+// makes the N-th device or pinned allocation fail as out of memory, launch:N the N-th HIP
+// call the runtime checks (kernel launches, copies, event calls) fail as a HIP error
+// without being made; counting starts when the variable takes its current value, which
+// the entry points that allocate or launch re-read once per call.  Unset, nothing is
+// counted.  Every kernel that is launched still runs to its normal end.
+enum FaultKind { kFaultNone = 0, kFaultAlloc = 1, kFaultLaunch = 2 };
+struct FaultState {
+    std::mutex mu;
+    std::string spec;
+    int kind = kFaultNone;
+    long n = 0, count = 0;
+};
+FaultState g_fault;
+std::atomic<int> g_fault_kind{kFaultNone};
+
+void fault_refresh() {
+    const char* v = std::getenv("SURROGATE_FAULT");
+    const std::string spec = v ? v : "";
+    std::lock_guard<std::mutex> lock(g_fault.mu);
+    if (spec == g_fault.spec) return;
+    g_fault.spec = spec;
+    g_fault.count = 0;
+    g_fault.kind = kFaultNone;
+    if (spec.rfind("alloc:", 0) == 0) g_fault.kind = kFaultAlloc;
+    if (spec.rfind("launch:", 0) == 0) g_fault.kind = kFaultLaunch;
+    g_fault.n = g_fault.kind == kFaultNone ? 0 : std::strtol(spec.c_str() + spec.find(':') + 1, nullptr, 10);
+    g_fault_kind.store(g_fault.kind);
+}
+
+bool fault(int kind) {
+    if (g_fault_kind.load(std::memory_order_relaxed) != kind) return false;
+    std::lock_guard<std::mutex> lock(g_fault.mu);
+    return g_fault.kind == kind && ++g_fault.count == g_fault.n;
+}
+
 #define SURR_HIP(expr)                                                                      \
     do {                                                                                    \
-        hipError_t e_ = (expr);                                                             \
+        hipError_t e_ = fault(kFaultLaunch) ? hipErrorLaunchFailure : (expr);               \
         if (e_ != hipSuccess)                                                               \
             return fail(SURR_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));     \
     } while (0)
@@ -198,6 +236,7 @@ surrogate_status run_chunks(surrogate_model* m, const int32_t* tokens_d, int64_t
 surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t row_stride,
                           const int32_t* lengths_h, int32_t batch, void* workspace_d,
                           size_t workspace_bytes, const PassIO& io, hipStream_t stream) {
+    fault_refresh();
     const surrogate_config& c = m->cfg;
     if (batch < 1) return fail(SURR_E_INVALID_ARG, "batch must be >= 1");
     if (row_stride < 1) return fail(SURR_E_INVALID_ARG, "row_stride must be >= 1");
@@ -285,8 +324,10 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
             if (m->pinned) SURR_HIP(hipHostFree(m->pinned));
             m->pinned = nullptr;
             m->pinned_bytes = 0;
-            if (hipHostMalloc(&m->pinned, meta_bytes, hipHostMallocDefault) != hipSuccess)
+            if (fault(kFaultAlloc) || hipHostMalloc(&m->pinned, meta_bytes, hipHostMallocDefault) != hipSuccess) {
+                m->pinned = nullptr;
                 return fail(SURR_E_OOM, "pinned staging buffer");
+            }
             m->pinned_bytes = meta_bytes;
         }
         char* P = static_cast<char*>(m->pinned);
@@ -305,8 +346,15 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
             std::memcpy(P + w.dec_first, dfirst.data(), 4 * dfirst.size());
             std::memcpy(P + w.dec_prompt, dprompt.data(), 4 * dprompt.size());
         }
-        SURR_HIP(hipMemcpyAsync(workspace_d, P, meta_bytes, hipMemcpyHostToDevice, stream));
-        SURR_HIP(hipEventRecord(m->staged, stream));
+        // Once the copy may be in flight, the buffer is not refilled before it is done: the
+        // event marks that, and if it cannot be recorded the stream is drained instead.
+        hipError_t e = fault(kFaultLaunch) ? hipErrorLaunchFailure
+                                           : hipMemcpyAsync(workspace_d, P, meta_bytes, hipMemcpyHostToDevice, stream);
+        if (e == hipSuccess) e = fault(kFaultLaunch) ? hipErrorLaunchFailure : hipEventRecord(m->staged, stream);
+        if (e != hipSuccess) {
+            hipStreamSynchronize(stream);
+            return fail(SURR_E_HIP, std::string("staging the batch plan: ") + hipGetErrorString(e));
+        }
         m->staged_pending = true;
     }
 
@@ -670,6 +718,7 @@ void surrogate_free(surrogate_model* m) {
 surrogate_status surrogate_load_weights_tensors(const surrogate_config* cfg, const void* const* tensors,
                                                 int32_t n_tensors, int32_t tensors_on_device,
                                                 hipStream_t stream, surrogate_model** out) {
+    fault_refresh();
     if (!cfg || !tensors || !out) return fail(SURR_E_INVALID_ARG, "null argument");
     *out = nullptr;
     std::string why;
@@ -707,7 +756,8 @@ surrogate_status surrogate_load_weights_tensors(const surrogate_config* cfg, con
     }
     const size_t o_fn = take(4 * d), o_head = take(mat(V, d));
     const size_t o_rope = take((size_t)c.max_pos * half * sizeof(float2)), o_err = take(4);
-    if (hipMalloc(&m->arena, off) != hipSuccess) {
+    if (fault(kFaultAlloc) || hipMalloc(&m->arena, off) != hipSuccess) {
+        m->arena = nullptr;
         surrogate_free(m);
         return fail(SURR_E_OOM, "weight arena of " + std::to_string(off) + " bytes");
     }
@@ -732,8 +782,10 @@ surrogate_status surrogate_load_weights_tensors(const surrogate_config* cfg, con
         };
         if (packed) {
             const size_t most = std::max({(dq + 2 * dkv) * d, d * dq, 2 * ff * d, d * ff, V * d}) * e;
-            if (hipMalloc(&stage, most) != hipSuccess)
+            if (fault(kFaultAlloc) || hipMalloc(&stage, most) != hipSuccess) {
+                stage = nullptr;
                 return fail(SURR_E_OOM, "weight staging buffer of " + std::to_string(most) + " bytes");
+            }
         }
         // matrix [rows, k] assembled at `rm` (row-major) by fill(rm), then placed at dst
         auto put = [&](void* dst, size_t rows, size_t k, auto fill) -> hipError_t {
@@ -889,6 +941,7 @@ surrogate_status surrogate_prefix_build(surrogate_model* m, const int32_t* token
                                         int32_t n_prefix, void* workspace_d,
                                         size_t workspace_bytes, hipStream_t stream,
                                         surrogate_prefix_cache** out) {
+    fault_refresh();
     if (!m || !tokens_d || !lengths_h || !workspace_d || !out) return fail(SURR_E_INVALID_ARG, "null argument");
     *out = nullptr;
     if (n_prefix < 1) return fail(SURR_E_INVALID_ARG, "n_prefix must be >= 1");
@@ -918,7 +971,7 @@ surrogate_status surrogate_prefix_build(surrogate_model* m, const int32_t* token
     for (int g = 0; g < n_prefix && st == SURR_OK; ++g)
         if (lengths_h[g] < 1 || lengths_h[g] > std::min<int64_t>(row_stride, m->cfg.max_pos - 1))
             st = fail(SURR_E_SHAPE, "length of prefix " + std::to_string(g) + " outside [1, min(row_stride, max_pos - 1)]");
-    if (st == SURR_OK && hipMalloc(&pc->mem, bytes) != hipSuccess) {
+    if (st == SURR_OK && (fault(kFaultAlloc) || hipMalloc(&pc->mem, bytes) != hipSuccess)) {
         pc->mem = nullptr;
         st = fail(SURR_E_OOM, "prefix cache of " + std::to_string(bytes) + " bytes");
     }
@@ -965,6 +1018,7 @@ surrogate_status surrogate_score_suffixes(surrogate_model* m, const surrogate_pr
 
 surrogate_status surrogate_cache_create(surrogate_model* m, int32_t n_entries,
                                         const int32_t* capacity_h, surrogate_prefix_cache** out) {
+    fault_refresh();
     if (!m || !capacity_h || !out) return fail(SURR_E_INVALID_ARG, "null argument");
     *out = nullptr;
     if (n_entries < 1) return fail(SURR_E_INVALID_ARG, "n_entries must be >= 1");
@@ -989,12 +1043,12 @@ surrogate_status surrogate_cache_create(surrogate_model* m, int32_t n_entries,
     pc->k_bytes = align_up((size_t)pc->rows * m->d_kv() * m->esz);
     pc->v_bytes = pc->k_bytes;
     const size_t bytes = (size_t)m->cfg.n_layers * (pc->k_bytes + pc->v_bytes);
-    if (hipMalloc(&pc->mem, bytes) != hipSuccess) {
+    if (fault(kFaultAlloc) || hipMalloc(&pc->mem, bytes) != hipSuccess) {
         delete pc;
         return fail(SURR_E_OOM, "cache of " + std::to_string(bytes) + " bytes");
     }
     // masked rows past an entry's length are still multiplied: they must be finite
-    if (hipMemset(pc->mem, 0, bytes) != hipSuccess) {
+    if (fault(kFaultLaunch) || hipMemset(pc->mem, 0, bytes) != hipSuccess) {
         hipFree(pc->mem);
         delete pc;
         return fail(SURR_E_HIP, "clearing the cache");
