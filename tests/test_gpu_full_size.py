@@ -39,10 +39,24 @@ def sha(a) -> str:
     return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
 
 
+def golden_meta(name, n_rows):
+    """The stored file's header; skips (naming the script that writes it) while the file
+    does not yet hold all n_rows rows: the oracle needs hours of CPU time for them."""
+    path = os.path.join(GOLDEN, name)
+    g = None
+    if os.path.exists(path):
+        with open(path) as f:
+            g = json.load(f)
+    if g is None or len(g["rows"]) < n_rows:
+        have = 0 if g is None else len(g["rows"])
+        pytest.skip(f"{name} holds {have} of {n_rows} stored oracle rows; "
+                    "write them with tests/golden/make_oracle_goldens.py")
+    return g
+
+
 def load_golden(name, shape, W, prompts):
     """Stored oracle rows, after checking they were computed on these very inputs."""
-    with open(os.path.join(GOLDEN, name)) as f:
-        g = json.load(f)
+    g = golden_meta(name, len(prompts))
     h = hashlib.sha256()
     for n in (s[0] for s in synth.tensor_specs(shape)):
         h.update(np.ascontiguousarray(W[n]).tobytes())
@@ -76,11 +90,10 @@ def check_selection(w, out, ref_conf=None, rows=None):
 @pytest.mark.timeout(900)
 def test_7b_config_full_batch_subset():
     w = synth.CONFIGS["7b"]
+    rows = golden_meta("oracle_7b_subset.json", 4)["row_index"]
     scorer, W = make_scorer(w.shape)
     tok, L = synth.make_prompts(w)
     vid = synth.verdict_ids(w)
-    with open(os.path.join(GOLDEN, "oracle_7b_subset.json")) as f:
-        rows = json.load(f)["row_index"]
     prompts = [tok[i, : L[i]] for i in rows]
     g, ref = load_golden("oracle_7b_subset.json", w.shape, W, prompts)
     print(f"7B workload: {len(L)} prompts, {int(L.sum())} tokens; oracle rows {rows} "
@@ -105,8 +118,7 @@ def test_14b_width_long_prompts():
     """Attention at the 14B workload's real lengths: the lazy re-base of the running
     maximum, the two-stage K/V ring and the longest-first work list over 8k-16k keys."""
     w = synth.CONFIGS["14b"]
-    with open(os.path.join(GOLDEN, "oracle_14b_long.json")) as f:
-        meta = json.load(f)
+    meta = golden_meta("oracle_14b_long.json", 4)
     shape = w.shape.replace(n_layers=meta["n_layers"])
     scorer, W = make_scorer(shape)
     tok, L = synth.make_prompts(w)
