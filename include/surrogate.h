@@ -29,9 +29,10 @@
  *    failed scoring, prefix or cache call leaves the model and its caches as they were
  *    (a failed cache_extend leaves its entries at their previous lengths).  For testing
  *    these paths, the environment variable SURROGATE_FAULT=alloc:N makes the N-th device
- *    or pinned allocation fail (SURR_E_OOM) and SURROGATE_FAULT=launch:N the N-th checked
- *    HIP call (SURR_E_HIP), counted from when the variable took its value; the calls
- *    that load weights, build prefixes, create caches or run a pass re-read it.
+ *    or pinned allocation of a call fail (SURR_E_OOM) and SURROGATE_FAULT=launch:N the
+ *    N-th checked HIP call of a call (SURR_E_HIP), counted from 1 in each call that loads
+ *    weights, builds prefixes, creates a cache or scores (score_pairs, score_suffixes,
+ *    cache_extend), each of which re-reads the variable; no other call is affected.
  */
 #ifndef SURROGATE_H
 #define SURROGATE_H

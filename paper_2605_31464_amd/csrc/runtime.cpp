@@ -30,44 +30,42 @@ surrogate_status fail(surrogate_status s, const std::string& msg) {
 }
 
 // Fault injection for the cleanup paths, forced from the host.  SURROGATE_FAULT=alloc:N
-// makes the N-th device or pinned allocation fail as out of memory, launch:N the N-th HIP
-// call the runtime checks (kernel launches, copies, event calls) fail as a HIP error
-// without being made; counting starts when the variable takes its current value, which
-// the entry points that allocate or launch re-read once per call.  Unset, nothing is
-// counted.  Every kernel that is launched still runs to its normal end.
+// makes the N-th device or pinned allocation of a call fail as out of memory, launch:N
+// the N-th HIP call the runtime checks (kernel launches, copies, event calls) fail as a
+// HIP error without being made.  Only the entry points that load weights, build
+// prefixes, create caches or run a pass count (each opens a FaultScope, which re-reads
+// the variable and starts counting at 1); every other call, and every call while the
+// variable is unset, is untouched.  Every kernel that is launched runs to its normal end.
 enum FaultKind { kFaultNone = 0, kFaultAlloc = 1, kFaultLaunch = 2 };
-struct FaultState {
-    std::mutex mu;
-    std::string spec;
-    int kind = kFaultNone;
-    long n = 0, count = 0;
-};
-FaultState g_fault;
-std::atomic<int> g_fault_kind{kFaultNone};
+thread_local int t_fault_depth = 0, t_fault_kind = kFaultNone;
+thread_local long t_fault_n = 0, t_fault_count = 0;
 
-void fault_refresh() {
-    const char* v = std::getenv("SURROGATE_FAULT");
-    const std::string spec = v ? v : "";
-    std::lock_guard<std::mutex> lock(g_fault.mu);
-    if (spec == g_fault.spec) return;
-    g_fault.spec = spec;
-    g_fault.count = 0;
-    g_fault.kind = kFaultNone;
-    if (spec.rfind("alloc:", 0) == 0) g_fault.kind = kFaultAlloc;
-    if (spec.rfind("launch:", 0) == 0) g_fault.kind = kFaultLaunch;
-    g_fault.n = g_fault.kind == kFaultNone ? 0 : std::strtol(spec.c_str() + spec.find(':') + 1, nullptr, 10);
-    g_fault_kind.store(g_fault.kind);
-}
+struct FaultScope {
+    FaultScope() {
+        if (t_fault_depth++ > 0) return;  // nested entry point: the outer call counts
+        const char* v = std::getenv("SURROGATE_FAULT");
+        const std::string spec = v ? v : "";
+        t_fault_kind = spec.rfind("alloc:", 0) == 0 ? kFaultAlloc
+                       : spec.rfind("launch:", 0) == 0 ? kFaultLaunch : kFaultNone;
+        t_fault_n = t_fault_kind == kFaultNone ? 0 : std::strtol(spec.c_str() + spec.find(':') + 1, nullptr, 10);
+        t_fault_count = 0;
+    }
+    ~FaultScope() {
+        if (--t_fault_depth == 0) t_fault_kind = kFaultNone;
+    }
+    FaultScope(const FaultScope&) = delete;
+    FaultScope& operator=(const FaultScope&) = delete;
+};
 
 bool fault(int kind) {
-    if (g_fault_kind.load(std::memory_order_relaxed) != kind) return false;
-    std::lock_guard<std::mutex> lock(g_fault.mu);
-    return g_fault.kind == kind && ++g_fault.count == g_fault.n;
+    return t_fault_depth > 0 && t_fault_kind == kind && ++t_fault_count == t_fault_n;
 }
 
 #define SURR_HIP(expr)                                                                      \
     do {                                                                                    \
-        hipError_t e_ = fault(kFaultLaunch) ? hipErrorLaunchFailure : (expr);               \
+        if (fault(kFaultLaunch))                                                            \
+            return fail(SURR_E_HIP, std::string("injected failure (SURROGATE_FAULT) of ") + #expr); \
+        hipError_t e_ = (expr);                                                             \
         if (e_ != hipSuccess)                                                               \
             return fail(SURR_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));     \
     } while (0)
@@ -236,7 +234,7 @@ surrogate_status run_chunks(surrogate_model* m, const int32_t* tokens_d, int64_t
 surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t row_stride,
                           const int32_t* lengths_h, int32_t batch, void* workspace_d,
                           size_t workspace_bytes, const PassIO& io, hipStream_t stream) {
-    fault_refresh();
+    FaultScope fault_scope;
     const surrogate_config& c = m->cfg;
     if (batch < 1) return fail(SURR_E_INVALID_ARG, "batch must be >= 1");
     if (row_stride < 1) return fail(SURR_E_INVALID_ARG, "row_stride must be >= 1");
@@ -348,12 +346,17 @@ surrogate_status run_pass(surrogate_model* m, const int32_t* tokens_d, int64_t r
         }
         // Once the copy may be in flight, the buffer is not refilled before it is done: the
         // event marks that, and if it cannot be recorded the stream is drained instead.
-        hipError_t e = fault(kFaultLaunch) ? hipErrorLaunchFailure
-                                           : hipMemcpyAsync(workspace_d, P, meta_bytes, hipMemcpyHostToDevice, stream);
-        if (e == hipSuccess) e = fault(kFaultLaunch) ? hipErrorLaunchFailure : hipEventRecord(m->staged, stream);
+        bool injected = fault(kFaultLaunch);
+        hipError_t e = injected ? hipErrorLaunchFailure
+                                : hipMemcpyAsync(workspace_d, P, meta_bytes, hipMemcpyHostToDevice, stream);
+        if (e == hipSuccess) {
+            injected = fault(kFaultLaunch);
+            e = injected ? hipErrorLaunchFailure : hipEventRecord(m->staged, stream);
+        }
         if (e != hipSuccess) {
             hipStreamSynchronize(stream);
-            return fail(SURR_E_HIP, std::string("staging the batch plan: ") + hipGetErrorString(e));
+            return fail(SURR_E_HIP, std::string("staging the batch plan: ") +
+                                        (injected ? "injected failure (SURROGATE_FAULT)" : hipGetErrorString(e)));
         }
         m->staged_pending = true;
     }
@@ -718,7 +721,7 @@ void surrogate_free(surrogate_model* m) {
 surrogate_status surrogate_load_weights_tensors(const surrogate_config* cfg, const void* const* tensors,
                                                 int32_t n_tensors, int32_t tensors_on_device,
                                                 hipStream_t stream, surrogate_model** out) {
-    fault_refresh();
+    FaultScope fault_scope;
     if (!cfg || !tensors || !out) return fail(SURR_E_INVALID_ARG, "null argument");
     *out = nullptr;
     std::string why;
@@ -941,7 +944,7 @@ surrogate_status surrogate_prefix_build(surrogate_model* m, const int32_t* token
                                         int32_t n_prefix, void* workspace_d,
                                         size_t workspace_bytes, hipStream_t stream,
                                         surrogate_prefix_cache** out) {
-    fault_refresh();
+    FaultScope fault_scope;
     if (!m || !tokens_d || !lengths_h || !workspace_d || !out) return fail(SURR_E_INVALID_ARG, "null argument");
     *out = nullptr;
     if (n_prefix < 1) return fail(SURR_E_INVALID_ARG, "n_prefix must be >= 1");
@@ -1018,7 +1021,7 @@ surrogate_status surrogate_score_suffixes(surrogate_model* m, const surrogate_pr
 
 surrogate_status surrogate_cache_create(surrogate_model* m, int32_t n_entries,
                                         const int32_t* capacity_h, surrogate_prefix_cache** out) {
-    fault_refresh();
+    FaultScope fault_scope;
     if (!m || !capacity_h || !out) return fail(SURR_E_INVALID_ARG, "null argument");
     *out = nullptr;
     if (n_entries < 1) return fail(SURR_E_INVALID_ARG, "n_entries must be >= 1");

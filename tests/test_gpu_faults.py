@@ -14,6 +14,7 @@ import numpy as np
 import pytest
 import torch
 
+from oracle import forecast as of
 from paper_2605_31464_amd import binding as B
 from paper_2605_31464_amd import synth
 
@@ -168,3 +169,31 @@ def test_prefix_and_cache_failures_release_their_memory(weights):
         assert failed >= 1
         if checked:
             assert free_bytes() >= base - SLACK
+
+
+def test_only_the_counting_entry_points_fail(weights):
+    """Calls outside loading, prefix building, cache creation and scoring passes never
+    count, with the variable set or left over from an earlier sweep."""
+    W, names = weights
+    scorer = B.Scorer(SHAPE, W, names, DEV)
+    tok, L = prompts()
+    out = scorer.score(tok, L, VID)
+    n = out["confidence"].numel()
+    rng = np.random.default_rng(4)
+    p8 = torch.from_numpy(rng.dirichlet(np.ones(8), 512).astype(np.float32)).to(DEV)
+    s8 = torch.from_numpy(np.exp(rng.normal(size=512)).astype(np.float32)).to(DEV)
+    m = [0.5, 0.9, 1.05, 1.2, 1.5, 2.0, 3.0, 5.0]
+    edges = list(of.HALF_OCTAVE_EDGES)  # the 7 interior edges of 8 bins
+    ref = (B.surrogate_select(out["confidence"], B.SURR_SELECT_BUDGET, budget_k=2),
+           B.surrogate_forecast_head(p8, m, edges, (1.5,)), B.surrogate_evaluate(p8, s8, m, edges))
+    for spec in ("launch:1", "alloc:1", "launch:2"):
+        os.environ["SURROGATE_FAULT"] = spec
+        got = (B.surrogate_select(out["confidence"], B.SURR_SELECT_BUDGET, budget_k=2),
+               B.surrogate_forecast_head(p8, m, edges, (1.5,)), B.surrogate_evaluate(p8, s8, m, edges))
+        (d, a, c), (d0, a0, c0) = got[0], ref[0]
+        assert torch.equal(c, c0), spec  # index lists are valid up to their counts
+        assert torch.equal(d[: int(c0[0])], d0[: int(c0[0])]) and torch.equal(a[: int(c0[1])], a0[: int(c0[1])])
+        for x, y in zip(got[1] + got[2], ref[1] + ref[2]):
+            assert (x is None and y is None) or torch.equal(x, y), spec
+    os.environ.pop("SURROGATE_FAULT")
+    assert n == len(L)
