@@ -136,8 +136,11 @@ surrogate_status surrogate_tensor_shape(const surrogate_config *cfg, int32_t ind
  * tensors in the order above; tensors[i] points to a dense row-major tensor of
  * surrogate_tensor_shape(i); all of them are host memory if tensors_on_device == 0, device
  * memory otherwise.  The library copies them into its own device arena (re-laid out for its
- * kernels), builds the RoPE cos/sin table in float64 and stores it as float32, and
- * synchronizes `stream` before returning, so the sources may be freed afterwards.
+ * kernels: bf16 projection matrices are stored in 256-row panels of 256 x 32 blocks, each
+ * placed through a transient device staging buffer of the largest matrix's size that is
+ * freed before returning), builds the RoPE cos/sin table in float64 and stores it as
+ * float32, and synchronizes `stream` before returning, so the sources may be freed
+ * afterwards.
  * Errors: SURR_E_INVALID_ARG (nulls), SURR_E_SHAPE (unsupported config),
  * SURR_E_WEIGHTS (n_tensors mismatch), SURR_E_OOM, SURR_E_HIP. */
 surrogate_status surrogate_load_weights_tensors(const surrogate_config *cfg,
