@@ -4,7 +4,8 @@
 // BM x BN workgroup tile of WM x WN wavefront tiles, K in steps of BK.  Both MFMA shapes
 // accumulate k in the same order and give bitwise the same sums.  Both operands are
 // K-contiguous, so one 16-byte chunk of a row is exactly the 8 consecutive k values an
-// MFMA lane supplies.  Tiles move from HBM straight into LDS with global_load_lds_dwordx4
+// MFMA lane supplies; the weight operand B is panel-packed (kernels.h), so the 16 rows one
+// wavefront load fetches are one 1 KB run.  Tiles move from HBM straight into LDS with global_load_lds_dwordx4
 // (no staging registers) through an NST-stage ring, one barrier per K step; LDS rows hold
 // BK/8 chunks whose order is XOR-swizzled by the row to spread the 16-byte reads over the
 // banks.  The MFMA is issued with the weight fragment as its A operand and the activation
