@@ -63,6 +63,7 @@ def check(p, S, m, edges, budgets=ev.PAPER_BUDGETS):
             assert got == pytest.approx(want, abs=1e-9), (c, got, want)
             exact.append(c)
         else:
+            # the summary is float64 on both sides: 1e-9 only absorbs its last-place rounding
             lo = 100 * float(S[sure_in].max()) / best if sure_in.any() else 0.0
             hi = 100 * float(S[sure_in | tied].max()) / best
             assert lo - 1e-9 <= got <= hi + 1e-9, (c, got, lo, hi)

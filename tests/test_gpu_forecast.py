@@ -63,12 +63,14 @@ def test_single_bin_and_optional_outputs():
     p = synth.bin_forecasts(100, 1, seed=4)
     s, disc = B.surrogate_forecast_head(torch.from_numpy(p).to(DEV), [2.5])
     assert disc is None
+    # one float32 product: |error| <= 2.5 * 2^-24 * p < 1.5e-7
     assert np.allclose(s.cpu().numpy(), 2.5 * p[:, 0], rtol=0, atol=1e-6)
     p8 = synth.bin_forecasts(50, 8, seed=5)
     s, disc = B.surrogate_forecast_head(torch.from_numpy(p8).to(DEV), of.table3_bin_values(0.2, 5.0),
                                         E8, (2.0,), want_speedup=False)
     assert s is None and disc.shape == (50, 1)
     want = of.discovery_score(p8.astype(np.float64), E8, 2.0)
+    # a float32 sum of at most 8 weighted probabilities, each <= 1: |error| <= 8 * 2^-23 < 1e-6
     assert np.abs(disc.cpu().numpy()[:, 0] - want).max() <= 1e-6
     empty = torch.empty(0, 8, dtype=torch.float32, device=DEV)
     s, disc = B.surrogate_forecast_head(empty, of.table3_bin_values(0.2, 5.0), E8, (2.0,))
@@ -127,6 +129,7 @@ def test_scored_eight_bin_forecasts_rank_like_the_oracle():
     tol = 1e-4 * np.abs(m).sum() + 1e-6
     assert np.abs(s.cpu().numpy() - s_ref).max() <= tol
     for c, x in enumerate((1.5, 2.0)):
+        # a sum of 8 bin probabilities, each within 1e-4 of the oracle, with weights <= 1
         assert np.abs(disc.cpu().numpy()[:, c] - of.discovery_score(ref["p"], E8, x)).max() <= 8e-4
     k = len(L) // 4
     d, a, cnt = B.surrogate_select(s, B.SURR_SELECT_TOP_SCORE, budget_k=k)
